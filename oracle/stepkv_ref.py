@@ -1,0 +1,303 @@
+"""Plain fp64 reference of StepKV's compression pass (test infrastructure only).
+
+Paper: "StepKV: Step-Aware KV Cache Compression for LLM Agents".
+
+Each function restates one definition of the paper in the paper's order and
+notation, with no blocking, fusion or streaming beyond what the definition
+states; numpy's matmul, exp and stable sort are the only library steps.
+Floating point is fp64 throughout, on values decoded exactly from bf16 bits.
+
+Readings taken where the paper is silent (the observation-window saliency is
+the reading fixed for this build; the paper calls T_i a conventional
+attention-based saliency, Sec. 5.2):
+
+* z[r, i] = scale * q_r . k_i for the window rows r = (w, g), w in [0, W),
+  g in [0, G), query head h*G + g; every cached key i of the sequence is
+  visible to every window row (no causal mask); scale = 1/sqrt(d).
+* A[i] = sum over rows r of the row-softmax of z (sum, not mean).
+* T = 1-D average pool of A restricted to prunable tokens: window k (odd),
+  stride 1, zero padding, divisor k, never crossing the sequence ends;
+  protected tokens contribute zero.
+* T_hat = T / max over prunable T (0 when that max is 0), so T_hat lies in
+  [0, 1] as the score-range analysis assumes (App. C.1).
+* P_i = alpha * T_hat_i + beta * S_{s(i)} for prunable i (eq. token-priority).
+* Keep the first min(B, N_pr) prunable tokens in a stable order by
+  (P descending, position ascending); NaN ranks as -inf and -0.0 as +0.0;
+  protected tokens are always kept and not counted in B (eq. problem).
+* Retained order is ascending position over protected and kept tokens.
+* Step utility follows Algorithm 1, phases 1 and 2, boundary by boundary;
+  gain_1 = 1 and red_1 = 0 by definition (Sec. 5.1.1); log is natural.
+
+Parity pins (tests/test_oracle_pins.py): every function below is pinned by
+closed forms, library routines it does not use, invariants or hand-derived
+values; none is "parity unpinned".
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+__all__ = [
+    "Params",
+    "decode_bf16",
+    "completion_score",
+    "step_utility",
+    "run_step_updates",
+    "budget_from_ratio",
+    "window_rows",
+    "window_attention",
+    "window_saliency",
+    "pooled_saliency",
+    "normalised_saliency",
+    "priority",
+    "select_retained",
+    "kept_per_step",
+    "step_statistics",
+    "compact",
+    "decode_attention",
+    "score_head",
+    "compress",
+]
+
+
+@dataclasses.dataclass
+class Params:
+    """Hyper-parameters; defaults are the paper's (App. D, hyper-parameter table)."""
+
+    alpha: float = 0.2  # token-saliency weight
+    beta: float = 0.8  # step-utility weight
+    pool_kernel: int = 7
+    scale: Optional[float] = None  # None -> 1/sqrt(d)
+    lam: float = 0.3  # redundancy penalty lambda
+    w_r: float = 0.85
+    w_c: float = 0.15
+    r_min: float = -1.0
+    r_max: float = 2.0
+    s_max: float = 8.0
+    eta: float = 1.5
+
+
+def decode_bf16(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) to float64; every bf16 value is exact in fp64."""
+    u = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return u.view(np.float32).astype(np.float64)
+
+
+# ---------------------------------------------------------------- step utility
+def completion_score(valid: float, gain: float, red: float, lam: float) -> float:
+    """eq. reward: r_k = valid_k + gain_k - lambda * red_k."""
+    return float(valid) + float(gain) - lam * float(red)
+
+
+def step_utility(r: float, c: float, p: Params) -> float:
+    """eq. step-score: S_k = clip(w_r clip(r_k, r_min, r_max) + w_c log(1 + c_k), 0, S_max)."""
+    inner = min(max(r, p.r_min), p.r_max)
+    val = p.w_r * inner + p.w_c * math.log(1.0 + c)
+    return min(max(val, 0.0), p.s_max)
+
+
+def run_step_updates(valid: Sequence[float], gain: Sequence[float], red: Sequence[float],
+                     obs_sim: np.ndarray, p: Params):
+    """Algorithm 1, phases 1-2, applied at the boundaries t = 1..n in turn.
+
+    Phase 1 scores the new step t (eq. reward) with c_t = 0 and sets S_t
+    (eq. step-score). Phase 2 raises c_k for every earlier step k by
+    min(1, eta * sim(Obs_t, Obs_k)) (eq. reuse) and recomputes S_k.
+    ``obs_sim[t, k]`` is sim(Obs_t, Obs_k) for k < t (0-based steps).
+    Returns (r, c, S) after the last boundary.
+    """
+    n = len(valid)
+    r = [0.0] * n
+    c = [0.0] * n
+    S = [0.0] * n
+    for t in range(n):
+        g = 1.0 if t == 0 else float(gain[t])  # gain_1 = 1
+        rd = 0.0 if t == 0 else float(red[t])  # red_1 = 0
+        r[t] = completion_score(valid[t], g, rd, p.lam)
+        c[t] = 0.0
+        S[t] = step_utility(r[t], c[t], p)
+        for k in range(t):
+            c[k] = c[k] + min(1.0, p.eta * float(obs_sim[t, k]))
+            S[k] = step_utility(r[k], c[k], p)
+    return np.array(r), np.array(c), np.array(S)
+
+
+def budget_from_ratio(rho: float, n_prunable: int) -> int:
+    """eq. problem: B_t = max(1, floor(rho * N_t)); 1e-9 absorbs fp error in rho*N."""
+    return max(1, int(math.floor(rho * n_prunable + 1e-9)))
+
+
+# ------------------------------------------------------------- token saliency
+def window_rows(q_win_ls: np.ndarray, h: int, group: int) -> np.ndarray:
+    """Window rows of KV head h: row r = w*G + g is query head h*G + g at window slot w.
+
+    q_win_ls: [W][Hq][d] (one layer, one sequence). Returns [W*G][d].
+    """
+    W, _, d = q_win_ls.shape
+    return q_win_ls[:, h * group:(h + 1) * group, :].reshape(W * group, d)
+
+
+def window_attention(q_rows: np.ndarray, keys: np.ndarray, scale: float) -> np.ndarray:
+    """Row-softmax of z = scale * Q K^T over all keys: p[r, i] (fp64)."""
+    z = (q_rows @ keys.T) * scale
+    m = z.max(axis=1, keepdims=True)
+    e = np.exp(z - m)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def window_saliency(q_rows: np.ndarray, keys: np.ndarray, scale: float) -> np.ndarray:
+    """A[i] = sum over window rows of the attention row-softmax (sums to W*G)."""
+    if keys.shape[0] == 0:
+        return np.zeros(0)
+    return window_attention(q_rows, keys, scale).sum(axis=0)
+
+
+def pooled_saliency(A: np.ndarray, prunable: np.ndarray, k: int) -> np.ndarray:
+    """T[i] = (1/k) * sum of A[j] * prunable[j] over |j - i| <= k // 2, 0 <= j < N."""
+    n = A.shape[0]
+    half = k // 2
+    a = np.where(prunable, A, 0.0)
+    T = np.zeros(n)
+    for off in range(-half, half + 1):
+        lo, hi = max(0, -off), min(n, n - off)
+        if lo < hi:
+            T[lo:hi] += a[lo + off:hi + off]
+    return T / k
+
+
+def normalised_saliency(T: np.ndarray, prunable: np.ndarray) -> np.ndarray:
+    """T_hat = T / max over prunable T, or 0 everywhere when that max is 0."""
+    if not prunable.any():
+        return np.zeros_like(T)
+    m = T[prunable].max()
+    if m <= 0.0:
+        return np.zeros_like(T)
+    return T / m
+
+
+def priority(T_hat: np.ndarray, step_ids: np.ndarray, S: np.ndarray, prunable: np.ndarray,
+             alpha: float, beta: float) -> np.ndarray:
+    """eq. token-priority: P_i = alpha T_i + beta S_{s(i)}; protected tokens get -inf.
+
+    A step id outside [0, len(S)) contributes utility 0.
+    """
+    n = T_hat.shape[0]
+    P = np.full(n, -np.inf)
+    ok = prunable & (step_ids >= 0) & (step_ids < S.shape[0])
+    util = np.zeros(n)
+    util[ok] = S[step_ids[ok]]
+    P[prunable] = alpha * T_hat[prunable] + beta * util[prunable]
+    return P
+
+
+def select_retained(P: np.ndarray, prunable: np.ndarray, budget: int) -> np.ndarray:
+    """Alg. 1 phase 3 and eq. problem: protected tokens plus the top-B prunable.
+
+    Ranking is a stable sort on (P descending, position ascending); NaN ranks
+    as -inf, -0.0 as +0.0. Exactly min(B, N_pr) prunable tokens are kept.
+    Returns the retained positions in ascending order (int64).
+    """
+    n = P.shape[0]
+    pos = np.arange(n)
+    cand = pos[prunable]
+    key = np.asarray(P, dtype=np.float64)[prunable].copy()
+    key[np.isnan(key)] = -np.inf
+    key[key == 0.0] = 0.0  # -0.0 -> +0.0
+    order = np.lexsort((cand, -key))
+    take = cand[order[:min(int(budget), cand.shape[0])]]
+    keep = np.zeros(n, dtype=bool)
+    keep[~prunable] = True
+    keep[take] = True
+    return pos[keep]
+
+
+def kept_per_step(idx: np.ndarray, step_ids: np.ndarray, prunable: np.ndarray,
+                  n_steps: int) -> np.ndarray:
+    """Number of retained prunable tokens of every step (a per-step histogram)."""
+    out = np.zeros(n_steps, dtype=np.int64)
+    for i in idx:
+        if prunable[i] and 0 <= step_ids[i] < n_steps:
+            out[step_ids[i]] += 1
+    return out
+
+
+def step_statistics(T_hat: np.ndarray, step_ids: np.ndarray, prunable: np.ndarray,
+                    n_steps: int) -> Dict[str, np.ndarray]:
+    """Per-step token count, max and sum of T_hat over the step's prunable tokens."""
+    cnt = np.zeros(n_steps, dtype=np.int64)
+    mx = np.zeros(n_steps)
+    sm = np.zeros(n_steps)
+    for i in range(T_hat.shape[0]):
+        k = step_ids[i]
+        if prunable[i] and 0 <= k < n_steps:
+            cnt[k] += 1
+            mx[k] = max(mx[k], T_hat[i])
+            sm[k] += T_hat[i]
+    return {"count": cnt, "max": mx, "sum": sm}
+
+
+def compact(K: np.ndarray, V: np.ndarray, idx: np.ndarray):
+    """eq. problem: C_hat = C_prot || C_traj[K], as rows gathered in position order."""
+    return K[idx], V[idx]
+
+
+def decode_attention(q: np.ndarray, K: np.ndarray, V: np.ndarray, scale: float) -> np.ndarray:
+    """One decode query against a (compacted) cache: softmax(scale q K^T) V."""
+    z = (K @ q) * scale
+    e = np.exp(z - z.max())
+    return (e / e.sum()) @ V
+
+
+# ------------------------------------------------------------- whole pass
+def score_head(q_rows: np.ndarray, keys: np.ndarray, step_ids: np.ndarray,
+               prunable: np.ndarray, S: np.ndarray, p: Params, scale: float):
+    """Saliency, pooling, normalisation and priority for one (sequence, layer, KV head)."""
+    A = window_saliency(q_rows, keys, scale)
+    T = pooled_saliency(A, prunable, p.pool_kernel)
+    T_hat = normalised_saliency(T, prunable)
+    P = priority(T_hat, step_ids, S, prunable, p.alpha, p.beta)
+    return A, T_hat, P
+
+
+def compress(q_win: np.ndarray, k: np.ndarray, v: Optional[np.ndarray], cu_seqlens: np.ndarray,
+             step_ids: np.ndarray, protected: np.ndarray, cu_steps: np.ndarray,
+             S: np.ndarray, budget: int, p: Params = Params(),
+             layers: Optional[Sequence[int]] = None, heads: Optional[Sequence[int]] = None,
+             seqs: Optional[Sequence[int]] = None, want_saliency: bool = False) -> Dict:
+    """Run the pass over the chosen (sequence, layer, KV head) triples, one at a time.
+
+    Arguments use the library's layouts with bf16 as uint16 bits:
+    q_win [L][S][W][Hq][d], k/v [L][Hkv][Ntot][d], step_ids/protected [Ntot],
+    S [cu_steps[-1]] (fp64 step utilities). Results are keyed by (s, l, h).
+    """
+    L, nseq, W, Hq, d = q_win.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    scale = p.scale if p.scale is not None else 1.0 / math.sqrt(d)
+    out: Dict = {"P": {}, "idx": {}, "T_hat": {}, "A": {}, "k_hat": {}, "v_hat": {},
+                 "kept": {}}
+    for s in (range(nseq) if seqs is None else seqs):
+        a, b = int(cu_seqlens[s]), int(cu_seqlens[s + 1])
+        sid = step_ids[a:b]
+        prun = protected[a:b] == 0
+        Ss = np.asarray(S[int(cu_steps[s]):int(cu_steps[s + 1])], dtype=np.float64)
+        for l in (range(L) if layers is None else layers):
+            qs = decode_bf16(q_win[l, s])
+            for h in (range(Hkv) if heads is None else heads):
+                keys = decode_bf16(k[l, h, a:b])
+                A, T_hat, P = score_head(window_rows(qs, h, G), keys, sid, prun, Ss, p, scale)
+                idx = select_retained(P, prun, budget)
+                key = (s, l, h)
+                out["P"][key] = P
+                out["idx"][key] = idx
+                out["kept"][key] = kept_per_step(idx, sid, prun, Ss.shape[0])
+                if want_saliency:
+                    out["A"][key] = A
+                    out["T_hat"][key] = T_hat
+                if v is not None and v.size:
+                    out["k_hat"][key] = k[l, h, a:b][idx]
+                    out["v_hat"][key] = v[l, h, a:b][idx]
+    return out

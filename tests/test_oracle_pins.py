@@ -1,0 +1,301 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself.
+
+Each test names the passage of the paper whose definition it pins and what
+fixes the expected value: a hand-evaluated closed form, an invariant, a
+library routine the oracle does not call, or a special case of the method
+that reduces to something simpler.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+import oracle as O
+from synth import f32_to_bf16_bits
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def bits(x):
+    return f32_to_bf16_bits(np.asarray(x, dtype=np.float32))
+
+
+# ------------------------------------------------------------- step utility
+def _golden_cases():
+    with open(os.path.join(GOLDEN, "step_utility.json")) as f:
+        return json.load(f)["cases"]
+
+
+@pytest.mark.parametrize("case", _golden_cases(), ids=lambda c: c["name"])
+def test_step_utility_hand_values(case):
+    """eq. reward / eq. reuse / eq. step-score in Algorithm 1's order (Sec. 5.1, App. C.3)."""
+    p = O.Params(**case["params"])
+    _, _, S = O.run_step_updates(case["valid"], case["gain"], case["red"],
+                                 np.array(case["obs_sim"], dtype=np.float64), p)
+    expect = [eval(e, {"log": math.log}) for e in case["expect_S"]]
+    np.testing.assert_allclose(S, expect, rtol=0, atol=1e-12)
+
+
+def test_reuse_accumulator_bounds():
+    """App. C.1: each reuse increment lies in [0, 1], so c_k >= 0 and grows by <= 1 a boundary."""
+    rng = np.random.default_rng(0)
+    n = 40
+    sim = np.tril(rng.random((n, n)), -1)
+    _, c, S = O.run_step_updates(np.ones(n), rng.random(n), rng.random(n), sim, O.Params())
+    assert (c >= 0).all()
+    for k in range(n):
+        assert c[k] <= (n - 1 - k) + 1e-12  # one increment per later boundary
+    assert (S >= 0).all() and (S <= 8).all()
+
+
+def test_budget_from_ratio():
+    """eq. problem: B_t = max(1, floor(rho N_t)); rho N computed in fp must not drop a unit."""
+    assert O.budget_from_ratio(0.2, 1000) == 200
+    assert O.budget_from_ratio(0.2, 3) == 1  # floor(0.6) = 0 -> max(1, 0)
+    assert O.budget_from_ratio(0.29, 100) == 29  # 0.29*100 = 28.999999999999996 in fp64
+    assert O.budget_from_ratio(0.5, 7) == 3
+
+
+# ------------------------------------------------------------- saliency
+def _rows_keys(W, G, d, N, seed):
+    rng = np.random.default_rng(seed)
+    q = O.decode_bf16(bits(rng.standard_normal((W * G, d))))
+    k = O.decode_bf16(bits(rng.standard_normal((N, d)) / math.sqrt(d)))
+    return q, k
+
+
+def test_saliency_zero_queries_is_uniform():
+    """With Q = 0 every row-softmax is uniform, so A_i = W*G/N exactly."""
+    _, k = _rows_keys(4, 3, 64, 37, 1)
+    A = O.window_saliency(np.zeros((12, 64)), k, 0.125)
+    np.testing.assert_allclose(A, np.full(37, 12 / 37), rtol=1e-15)
+
+
+def test_saliency_two_level_closed_form():
+    """Keys on one axis give two logit levels; the softmax has a closed form."""
+    d, N, W, G = 64, 50, 8, 2
+    scale = 1.0 / math.sqrt(d)
+    c, a, b = 3.0, 1.5, -0.5
+    q = np.zeros((W * G, d))
+    q[:, 0] = c
+    k = np.zeros((N, d))
+    hi = np.arange(N) % 5 == 0  # 10 keys at level a, 40 at level b
+    k[hi, 0] = a
+    k[~hi, 0] = b
+    A = O.window_saliency(q, k, scale)
+    za, zb = c * a * scale, c * b * scale
+    den = 10 * math.exp(za) + 40 * math.exp(zb)
+    expect = np.where(hi, W * G * math.exp(za) / den, W * G * math.exp(zb) / den)
+    np.testing.assert_allclose(A, expect, rtol=1e-13)
+
+
+def test_saliency_matches_library_softmax():
+    """A = column sums of softmax(scale Q K^T) (scipy and torch softmax, not the oracle's exp)."""
+    q, k = _rows_keys(16, 4, 128, 301, 2)
+    scale = 1.0 / math.sqrt(128)
+    z = (q @ k.T) * scale
+    ref_scipy = scipy.special.softmax(z, axis=1).sum(axis=0)
+    ref_torch = torch.softmax(torch.from_numpy(z), dim=1).sum(dim=0).numpy()
+    A = O.window_saliency(q, k, scale)
+    np.testing.assert_allclose(A, ref_scipy, rtol=1e-12)
+    np.testing.assert_allclose(A, ref_torch, rtol=1e-12)
+
+
+def test_saliency_invariants():
+    """A >= 0 and sum_i A_i = W*G (each row-softmax sums to one)."""
+    q, k = _rows_keys(32, 4, 128, 999, 3)
+    A = O.window_saliency(q, k * 5.0, 1.0 / math.sqrt(128))
+    assert (A >= 0).all()
+    assert abs(A.sum() - 128) < 1e-10
+
+
+def test_gqa_row_mapping():
+    """Query head h_q reads KV head floor(h_q / G); window row r = w*G + g."""
+    W, Hq, Hkv, d = 3, 4, 2, 64
+    G = Hq // Hkv
+    q = np.zeros((W, Hq, d))
+    q[1, 1, 5] = 40.0  # query head 1 -> KV head 0, window slot 1
+    rows0 = O.window_rows(q, 0, G)
+    rows1 = O.window_rows(q, 1, G)
+    assert rows0.shape == (W * G, d)
+    assert rows0[1 * G + 1, 5] == 40.0 and np.count_nonzero(rows0) == 1
+    assert np.count_nonzero(rows1) == 0
+    k = np.zeros((20, d))
+    k[7, 5] = 1.0
+    A0 = O.window_saliency(rows0, k, 1.0)
+    A1 = O.window_saliency(rows1, k, 1.0)
+    np.testing.assert_allclose(A1, np.full(20, W * G / 20), rtol=1e-15)
+    assert A0.argmax() == 7 and A0[7] > W * G / 20 + 0.9
+
+
+def test_saliency_brute_force_loops():
+    """Pure-Python loops with math.exp on a tiny case (a second, unvectorised reading)."""
+    q, k = _rows_keys(4, 2, 64, 23, 4)
+    scale = 0.125
+    A = [0.0] * 23
+    for r in range(8):
+        z = [scale * sum(q[r, j] * k[i, j] for j in range(64)) for i in range(23)]
+        m = max(z)
+        e = [math.exp(x - m) for x in z]
+        t = sum(e)
+        for i in range(23):
+            A[i] += e[i] / t
+    np.testing.assert_allclose(O.window_saliency(q, k, scale), A, rtol=1e-12)
+
+
+# ------------------------------------------------------------- pooling, normalisation
+def test_pool_constant_closed_form():
+    """Constant A on prunable tokens: interior T = A, an edge with e missing taps gives A(k-e)/k."""
+    n, k = 30, 7
+    A = np.full(n, 2.0)
+    T = O.pooled_saliency(A, np.ones(n, bool), k)
+    np.testing.assert_allclose(T[3:-3], 2.0, rtol=1e-15)
+    for e in range(1, 4):
+        np.testing.assert_allclose(T[3 - e], 2.0 * (k - e) / k, rtol=1e-15)
+        np.testing.assert_allclose(T[n - 4 + e], 2.0 * (k - e) / k, rtol=1e-15)
+
+
+def test_pool_impulse_response_and_protected_mask():
+    """An impulse spreads A_j/k over exactly [j-3, j+3]; protected tokens contribute nothing."""
+    n = 40
+    A = np.zeros(n)
+    A[20] = 7.0
+    A[2] = 100.0  # protected below
+    prun = np.ones(n, bool)
+    prun[:5] = False
+    T = O.pooled_saliency(A, prun, 7)
+    expect = np.zeros(n)
+    expect[17:24] = 1.0
+    np.testing.assert_allclose(T, expect, rtol=1e-15, atol=0)
+
+
+def test_normalisation_uses_prunable_max():
+    """T_hat in [0, 1] with 1 at the prunable argmax; a large protected value does not flatten it."""
+    T = np.array([50.0, 1.0, 4.0, 2.0, 0.0])
+    prun = np.array([False, True, True, True, True])
+    Th = O.normalised_saliency(T, prun)
+    np.testing.assert_allclose(Th[1:], [0.25, 1.0, 0.5, 0.0], rtol=1e-15)
+    assert (O.normalised_saliency(np.zeros(4), np.ones(4, bool)) == 0).all()
+
+
+# ------------------------------------------------------------- priority and selection
+def test_priority_range_and_dominance():
+    """App. C.1: Score in [0, alpha H_max + beta U_max]; the step preference flips exactly
+    where alpha (H_i - H_j) = beta (U_s(j) - U_s(i))."""
+    S = np.array([0.5, 1.0])
+    sid = np.array([0, 1])
+    prun = np.ones(2, bool)
+    alpha, beta = 0.2, 0.8
+    # token 0 (step utility 0.5) out-salients token 1 (utility 1.0) by dH
+    # threshold dH* = beta (1.0 - 0.5) / alpha = 2 > 1, so within [0,1] the step wins
+    P = O.priority(np.array([1.0, 0.0]), sid, S, prun, alpha, beta)
+    assert P[1] > P[0]
+    P = O.priority(np.array([1.0, 0.0]), sid, np.array([0.5, 0.6]), prun, alpha, beta)
+    # dH = 1 > beta*0.1/alpha = 0.4 -> token saliency wins
+    assert P[0] > P[1]
+    rng = np.random.default_rng(5)
+    Th = rng.random(100)
+    Sr = rng.random(10) * 8
+    P = O.priority(Th, rng.integers(0, 10, 100), Sr, np.ones(100, bool), alpha, beta)
+    assert P.min() >= 0 and P.max() <= alpha * 1 + beta * 8
+
+
+def _brute_select(P, prun, B):
+    """Python's sorted() on (-P, i): a different sort routine from the oracle's lexsort."""
+    cand = [i for i in range(len(P)) if prun[i]]
+
+    def key(i):
+        x = float(P[i])
+        if math.isnan(x):
+            x = -math.inf
+        return (-x, i)
+
+    take = sorted(cand, key=key)[:min(B, len(cand))]
+    return sorted(set(take) | {i for i in range(len(P)) if not prun[i]})
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_select_matches_python_sorted(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 300))
+    P = np.round(rng.random(n) * 5) / 5  # many exact ties
+    P[rng.random(n) < 0.05] = np.nan
+    P[rng.random(n) < 0.05] = -0.0
+    prun = rng.random(n) > 0.2
+    B = int(rng.integers(1, n + 5))
+    idx = O.select_retained(P, prun, B)
+    assert list(idx) == _brute_select(P, prun, B)
+    assert (np.diff(idx) > 0).all()
+    assert int(prun[idx].sum()) == min(B, int(prun.sum()))
+    assert set(np.nonzero(~prun)[0]) <= set(idx)
+
+
+def test_select_alpha_zero_takes_whole_steps():
+    """alpha = 0 (no token score, Table 3): whole steps in descending S, lowest positions first."""
+    sid = np.repeat(np.arange(4), 10)
+    S = np.array([0.3, 1.2, 0.7, 1.2])
+    prun = np.ones(40, bool)
+    P = O.priority(np.random.default_rng(1).random(40), sid, S, prun, 0.0, 0.8)
+    idx = O.select_retained(P, prun, 25)
+    expect = list(range(10, 20)) + list(range(30, 40)) + list(range(20, 25))
+    assert list(idx) == sorted(expect)
+
+
+def test_select_beta_zero_is_saliency_topk():
+    """beta = 0 (no step score, Table 3): the plain top-B of T_hat."""
+    rng = np.random.default_rng(2)
+    Th = rng.random(200)
+    sid = rng.integers(0, 5, 200)
+    prun = np.ones(200, bool)
+    P = O.priority(Th, sid, rng.random(5), prun, 0.2, 0.0)
+    idx = O.select_retained(P, prun, 30)
+    assert set(idx) == set(np.argsort(-Th)[:30])
+
+
+def test_select_all_equal_and_budget_edges():
+    prun = np.array([0, 0, 1, 1, 1, 1, 1], bool)
+    P = np.zeros(7)
+    assert list(O.select_retained(P, prun, 2)) == [0, 1, 2, 3]
+    assert list(O.select_retained(P, prun, 99)) == list(range(7))
+    assert list(O.select_retained(P, np.zeros(7, bool), 3)) == list(range(7))  # all protected
+    assert list(O.select_retained(P, ~np.zeros(7, bool), 0)) == []
+
+
+def test_kept_per_step_sums_to_kept():
+    rng = np.random.default_rng(3)
+    sid = np.concatenate([np.full(5, -1), np.repeat(np.arange(6), 9)])
+    prun = sid >= 0
+    P = O.priority(rng.random(59), sid, rng.random(6), prun, 0.2, 0.8)
+    idx = O.select_retained(P, prun, 17)
+    kept = O.kept_per_step(idx, sid, prun, 6)
+    assert kept.sum() == 17
+    st = O.step_statistics(rng.random(59), sid, prun, 6)
+    assert (st["count"] == 9).all()
+
+
+# ------------------------------------------------------------- compaction, decode
+def test_compact_is_row_gather():
+    rng = np.random.default_rng(4)
+    K = rng.integers(0, 65535, (50, 8), dtype=np.uint16)
+    V = rng.integers(0, 65535, (50, 8), dtype=np.uint16)
+    idx = np.array([0, 3, 4, 17, 49])
+    kh, vh = O.compact(K, V, idx)
+    for j, i in enumerate(idx):
+        assert (kh[j] == K[i]).all() and (vh[j] == V[i]).all()
+
+
+def test_decode_attention_matches_torch_sdpa():
+    rng = np.random.default_rng(6)
+    K = rng.standard_normal((33, 64))
+    V = rng.standard_normal((33, 64))
+    q = rng.standard_normal(64)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None, None, None], torch.from_numpy(K)[None, None],
+        torch.from_numpy(V)[None, None]).numpy().reshape(-1)
+    np.testing.assert_allclose(O.decode_attention(q, K, V, 1 / 8), ref, rtol=1e-12)
+    # one retained row: the output is that value row
+    np.testing.assert_allclose(O.decode_attention(q, K[:1], V[:1], 1 / 8), V[0], rtol=1e-15)
