@@ -1,0 +1,216 @@
+#!/usr/bin/env python3
+"""Throughput of the StepKV compression pass on one MI355X.
+
+One step = the whole pass over one synthetic batch: host step-utility update
+(Algorithm 1 phases 1-2) -> saliency -> priority -> top-B select -> K/V
+compaction, all layers and KV heads. Inputs are resident in HBM before the
+timed region. Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload l32_32k] [--budget 1024]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "KV tokens compressed/sec (all layers) + achieved HBM GB/s vs peak, 32k ctx"
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="l32_32k")
+    ap.add_argument("--budget", type=int, default=None)
+    ap.add_argument("--window", type=int, default=None)
+    ap.add_argument("--layers", type=int, default=None)
+    ap.add_argument("--seed", type=int, default=233)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="budget for the oracle CPU baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, budget, seconds):
+    """Time the oracle on whole (sequence, layer, KV head) triples until `seconds` pass."""
+    import oracle as O
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    S = np.concatenate([O.run_step_updates(g.valid, g.gain, g.red, g.obs_sim.astype(np.float64),
+                                           O.Params())[2] for g in w.signals])
+    triples = [(s, l, h) for l in range(w.num_layers) for h in range(w.num_kv_heads)
+               for s in range(w.num_seqs)]
+    rng = np.random.default_rng(0)
+    rng.shuffle(triples)
+    done, tokens, t0 = 0, 0, time.perf_counter()
+    for s, l, h in triples:
+        O.compress(w.q_win, w.k, w.v, w.cu_seqlens, w.step_ids, w.protected, w.cu_steps, S,
+                   budget, O.Params(), layers=[l], heads=[h], seqs=[s])
+        done += 1
+        tokens += w.seqlens[s]
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    # whole-job rate: every token is scored in all L x Hkv heads
+    per_head_rate = tokens / dt
+    value = per_head_rate / (w.num_layers * w.num_kv_heads)
+    return {"value": value, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} of {len(triples)} (sequence, layer, KV head) triples "
+                      f"({tokens} token-heads) in {dt:.1f} s, scaled to all {w.num_layers} layers "
+                      f"x {w.num_kv_heads} KV heads"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}): "
+              "the compression pass is independent per (layer, KV head) and this build has no "
+              "multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    from synth import make_workload
+
+    t_gen = time.perf_counter()
+    kw = {}
+    if args.window:
+        kw["window"] = args.window
+    if args.layers:
+        kw["num_layers"] = args.layers
+    w = make_workload(args.workload, args.seed, **kw)
+    budget = args.budget or w.budget
+    print(f"# generated {args.workload} in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr,
+          flush=True)
+
+    import torch
+
+    from paper_2609_22158_amd import binding as B
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    pb = B.Problem.from_workload(w, dev)
+    q, k, v = (B.bf16_from_bits(x, dev) for x in (w.q_win, w.k, w.v))
+    sid = torch.from_numpy(w.step_ids).to(dev)
+    prot = torch.from_numpy(w.protected).to(dev)
+    util = torch.empty(pb.total_steps, dtype=torch.float32, device=dev)
+    util_pinned = torch.empty(pb.total_steps, dtype=torch.float32, pin_memory=True)
+    L, Hkv, ntot, d = w.num_layers, w.num_kv_heads, w.total_tokens, w.head_dim
+    sal = torch.empty((L, Hkv, ntot), dtype=torch.float32, device=dev)
+    scores = torch.empty_like(sal)
+    idx = torch.empty((L, Hkv, ntot), dtype=torch.int32, device=dev)
+    cu_ret = torch.empty(w.num_seqs + 1, dtype=torch.int32, device=dev)
+    out_rows = B.retained_rows(w.seqlens, w.protected_len, budget)
+    k_out = torch.empty((L, Hkv, out_rows, d), dtype=torch.bfloat16, device=dev)
+    v_out = torch.empty_like(k_out)
+    ws = torch.empty(pb.saliency_workspace_bytes(), dtype=torch.uint8, device=dev)
+    params = B.Params()
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        # a0: host step utility (Algorithm 1 phases 1-2) for every sequence
+        S = np.concatenate([B.step_utilities(g.valid, g.gain, g.red, g.obs_sim)
+                            for g in w.signals])
+        util_pinned.numpy()[:] = S
+        util.copy_(util_pinned, non_blocking=True)
+        if ev:
+            ev[0].record(stream)
+        B.saliency(pb, q, k, params, workspace=ws, out=sal)
+        if ev:
+            ev[1].record(stream)
+        B.priority(pb, sal, sid, prot, util, params, scores=scores)
+        if ev:
+            ev[2].record(stream)
+        B.select(pb, scores, prot, sid, budget, idx=idx, cu_retained=cu_ret)
+        if ev:
+            ev[3].record(stream)
+        B.compact(pb, k, v, idx, cu_ret, out_rows, k_out=k_out, v_out=v_out)
+        if ev:
+            ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    assert int(cu_ret[-1].item()) == out_rows
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+    ms_per_step = max(total_ms, wall * 1e3) / args.steps
+    stage_names = ["saliency", "priority", "select", "compact"]
+    stage_ms = {n: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
+                for i, n in enumerate(stage_names)}
+
+    tokens = float(ntot)
+    value = tokens / (ms_per_step * 1e-3)
+    G = w.num_q_heads // Hkv
+    R = w.window * G
+    lh = L * Hkv
+    # algorithmic work per launch
+    k_bytes = lh * ntot * d * 2
+    sal_flops = 2 * 2 * R * d * ntot * lh            # two sweeps of Q K^T
+    sal_bytes = k_bytes + lh * ntot * 4 + q.numel() * 2  # K once, A written, Q read
+    compact_bytes = lh * out_rows * d * 2 * 2 * 2     # K and V rows, read and written
+    t_sal = stage_ms["saliency"] * 1e-3
+    t_cmp = stage_ms["compact"] * 1e-3
+    achieved_tflops = sal_flops / t_sal / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved_tflops, 2),
+                "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved_tflops / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "kernel": "saliency (two MFMA sweeps over K)"}
+    hbm = {"saliency_gbps": round(sal_bytes / t_sal / 1e9, 1),
+           "saliency_frac": round(sal_bytes / t_sal / 1e9 / HBM_PEAK_GBS, 4),
+           "compact_gbps": round(compact_bytes / t_cmp / 1e9, 1),
+           "compact_frac": round(compact_bytes / t_cmp / 1e9 / HBM_PEAK_GBS, 4),
+           "peak_gbps": HBM_PEAK_GBS}
+
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {L} layers, {w.num_q_heads} query / {Hkv} KV "
+                               f"heads, d {d}, {w.num_seqs} sequence(s) of {w.seqlens[:4]}"
+                               f"{'...' if w.num_seqs > 4 else ''} tokens, window {w.window}, "
+                               f"budget {budget} per KV head",
+                   "layers": L, "kv_heads": Hkv, "q_heads": w.num_q_heads, "head_dim": d,
+                   "seq_len": int(max(w.seqlens)), "tokens": int(ntot), "window": w.window,
+                   "budget": budget, "seed": args.seed},
+        "entries_per_s": round(value * lh, 1),
+        "stages_ms": {n: round(x, 4) for n, x in stage_ms.items()},
+        "hbm": hbm,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, budget, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

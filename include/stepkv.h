@@ -1,0 +1,241 @@
+/*
+ * stepkv.h - C ABI of the StepKV compression pass on AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "StepKV: Step-Aware KV Cache Compression for LLM Agents".
+ *
+ * At a post-step pruning boundary (Sec. 3) the KV cache of every sequence is
+ * C = C_prot || C_traj. The pass scores every cached token of every layer and
+ * KV head, keeps the protected tokens plus the top-B prunable ones, and
+ * rewrites the cache densely (eq. problem):
+ *
+ *   stepkv_score    window saliency T_i fused with step utility S_k into the
+ *                   retention priority P_i = alpha*T_i + beta*S_k
+ *                   (Sec. 5.2, eq. token-priority); it is the composition of
+ *                   stepkv_saliency (the attention sweeps over K) and
+ *                   stepkv_priority (pooling, normalisation, fusion)
+ *   stepkv_select   global top-B ranking per (sequence, layer, KV head)
+ *                   (Sec. 5.2 last paragraph; Algorithm 1 phase 3)
+ *   stepkv_compact  C_hat = C_prot || C_traj[K] (eq. problem)
+ *
+ * Host-only helpers implement the budget rule B_t = max(1, floor(rho N_t))
+ * (eq. problem) and the step-utility update of Algorithm 1 phases 1-2
+ * (eq. reward, eq. reuse, eq. step-score).
+ *
+ * Conventions for every call:
+ *  - Tensor pointers are DEVICE pointers unless the name ends in _host. The
+ *    caller owns every buffer; the library never allocates device memory and
+ *    keeps no global state, so calls are re-entrant given distinct workspaces.
+ *  - Device work is enqueued on `stream` (a hipStream_t; NULL = default
+ *    stream) and is asynchronous: a return of STEPKV_OK means validation
+ *    passed and every kernel was launched.
+ *  - bf16 tensors hold raw bfloat16 values (2 bytes each).
+ *  - Arguments are validated on the host before anything is launched; a
+ *    failed validation returns an error code and launches nothing.
+ *  - No C++ exception crosses this interface.
+ *
+ * Layouts (L layers, S sequences, Hq query heads, Hkv KV heads, G = Hq/Hkv,
+ * d head dim, W window length, Ntot = cu_seqlens[S]):
+ *  q_win        bf16  [L][S][W][Hq][d]   last W queries of every sequence
+ *  k, v         bf16  [L][Hkv][Ntot][d]  sequences concatenated along Ntot
+ *  step_ids     int32 [Ntot]             step index local to the sequence
+ *  protected    uint8 [Ntot]             nonzero = protected (never pruned)
+ *  step_utility fp32  [cu_steps[S]]      S_k of sequence s at cu_steps[s] + k
+ *  scores       fp32  [L][Hkv][Ntot]     P_i (protected tokens: -inf)
+ *  saliency     fp32  [L][Hkv][Ntot]     A_i, the raw window saliency
+ *  idx          int32 [L][Hkv][Ntot]     retained positions of sequence s
+ *                                        (local, ascending) at offset
+ *                                        cu_seqlens[s] of every (l, h) row
+ *  cu_retained  int32 [S+1]              prefix sums of retained rows per
+ *                                        sequence (same for every (l, h))
+ *  k_out, v_out bf16  [L][Hkv][out_rows][d]  compacted cache; sequence s
+ *                                        occupies rows cu_retained[s] ...
+ */
+#ifndef STEPKV_H_
+#define STEPKV_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- errors */
+#define STEPKV_OK 0
+#define STEPKV_EINVAL (-1)       /* null pointer, bad shape or parameter */
+#define STEPKV_EUNSUPPORTED (-2) /* valid but outside this build's limits */
+#define STEPKV_EWORKSPACE (-3)   /* workspace missing or too small */
+#define STEPKV_EHIP (-4)         /* a HIP launch or runtime call failed */
+
+/* Limits of this build (STEPKV_EUNSUPPORTED beyond them). */
+#define STEPKV_MAX_WINDOW_ROWS 256   /* W * G */
+#define STEPKV_MAX_POOL_KERNEL 63    /* odd pooling window */
+#define STEPKV_MAX_STEPS_STATS 4096  /* steps per sequence when stats are requested */
+
+/* ---------------------------------------------------------------- types */
+/* Shape of one compression problem: a batch of S sequences, all layers. */
+typedef struct stepkv_problem {
+  int32_t num_layers;   /* L >= 1 */
+  int32_t num_q_heads;  /* Hq >= 1, a multiple of num_kv_heads */
+  int32_t num_kv_heads; /* Hkv >= 1 */
+  int32_t head_dim;     /* d: 64 or 128 */
+  int32_t window;       /* W >= 1 observation-window queries */
+  int32_t num_seqs;     /* S >= 1 */
+  const int32_t* cu_seqlens_host; /* [S+1] host: 0 = cu[0] <= cu[1] <= ... */
+  const int32_t* cu_seqlens;      /* [S+1] device copy of the same values */
+  const int32_t* cu_steps_host;   /* [S+1] host: offsets into step_utility */
+  const int32_t* cu_steps;        /* [S+1] device copy of the same values */
+} stepkv_problem;
+
+/* Method parameters; stepkv_params_default() fills the paper's defaults
+ * (hyper-parameter table, App. D). */
+typedef struct stepkv_params {
+  float alpha;          /* token-saliency weight (0.2) */
+  float beta;           /* step-utility weight (0.8) */
+  int32_t pool_kernel;  /* odd 1-D average-pool window over A (7) */
+  float scale;          /* softmax scale; <= 0 selects 1/sqrt(d) */
+  /* step utility (Sec. 5.1) */
+  float lambda_red;     /* redundancy penalty lambda (0.3) */
+  float w_r, w_c;       /* completion / reuse weights (0.85, 0.15) */
+  float r_min, r_max;   /* completion-score clip (-1, 2) */
+  float s_max;          /* utility clip S_max (8) */
+  float eta;            /* reuse update scale (1.5) */
+} stepkv_params;
+
+/* Per-step statistics of one (layer, KV head, step), from stepkv_score:
+ * over the step's prunable tokens, their count, the max of the normalised
+ * saliency T_hat, and its sum in unsigned fixed point with 32 fractional bits
+ * (sum = sum_q32 / 2^32), accumulated order-independently. */
+typedef struct stepkv_step_stat {
+  uint32_t count;
+  float max_saliency;
+  uint64_t sum_saliency_q32;
+} stepkv_step_stat;
+
+/* Step-utility state of one trajectory for the host update (Algorithm 1
+ * phases 1-2). Arrays are caller-owned with room for `capacity` steps. */
+typedef struct stepkv_step_state {
+  int32_t capacity;  /* entries available in r and c */
+  int32_t num_steps; /* t: completed steps so far (start at 0) */
+  double* r;         /* completion score r_k (eq. reward) */
+  double* c;         /* reuse accumulator c_k (eq. reuse) */
+} stepkv_step_state;
+
+/* ---------------------------------------------------------------- host helpers */
+/* Fill the paper's default parameters (App. D hyper-parameter table) and the
+ * 1-D pooling window 7. Never fails for a non-null pointer. */
+void stepkv_params_default(stepkv_params* prm);
+
+/* Static text for an error code. */
+const char* stepkv_strerror(int code);
+
+/* eq. problem: B = max(1, floor(rho * n_prunable)), rho in (0, 1].
+ * Returns -1 for rho outside (0, 1] or n_prunable < 0. */
+int64_t stepkv_budget_from_ratio(double rho, int64_t n_prunable);
+
+/* Algorithm 1 phases 1-2 at the boundary after step t = state->num_steps + 1.
+ * Phase 1: r_t = valid + gain - lambda*red (eq. reward; for the first step
+ * gain = 1 and red = 0 by definition), c_t = 0. Phase 2: for k < t,
+ * c_k += min(1, eta * obs_sim_prev[k]) (eq. reuse), where obs_sim_prev[k] is
+ * sim(Obs_t, Obs_k) (host, t-1 entries; may be NULL when t = 1). Then writes
+ * S_k = clip(w_r clip(r_k, r_min, r_max) + w_c ln(1 + c_k), 0, S_max)
+ * (eq. step-score) for all k <= t into S_out (host, >= t floats).
+ * Returns STEPKV_EINVAL for null state/params/S_out, a full state, or a
+ * similarity outside [0, 1] or non-finite signal. O(t), host only. */
+int stepkv_step_update(stepkv_step_state* state, float valid, float gain, float red,
+                       const float* obs_sim_prev, const stepkv_params* prm, float* S_out);
+
+/* ---------------------------------------------------------------- device passes */
+/* Bytes of device workspace stepkv_score needs for this problem (0 when the
+ * problem is invalid). The workspace needs no initialisation and is
+ * scratch between calls; 256-byte alignment is required. */
+size_t stepkv_score_workspace_bytes(const stepkv_problem* pb);
+
+/* Bytes of device workspace stepkv_saliency needs (0 when invalid); never
+ * more than stepkv_score_workspace_bytes. Same rules. */
+size_t stepkv_saliency_workspace_bytes(const stepkv_problem* pb);
+
+/* Sec. 5.2, token saliency: the raw observation-window saliency
+ *   A_i = sum_r softmax_i(scale * q_r . k_i)
+ * of every token, for every (sequence, layer, KV head), written to saliency
+ * fp32 [L][Hkv][Ntot]. Window rows r = w*G + g use query head h*G + g; all
+ * N_s keys of the sequence are visible. Computed exactly (two sweeps over K:
+ * row log-sum-exp, then column sums), fp32 accumulation of bf16 products.
+ * Errors: EINVAL (null pointers, bad problem or scale), EUNSUPPORTED (d not in
+ * {64,128} or W*G > STEPKV_MAX_WINDOW_ROWS), EWORKSPACE, EHIP. */
+int stepkv_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                    const void* k, float* saliency, void* workspace, size_t ws_bytes,
+                    void* stream);
+
+/* Sec. 5.2, eq. token-priority, from a saliency computed by stepkv_saliency:
+ *   T_i = (1/k) sum_{|j-i| <= k/2} A_j [j prunable], zero padding, per sequence
+ *   Th_i = T_i / max_{prunable} T  (0 when that max is 0)
+ *   P_i  = alpha * Th_i + beta * S_{step_ids[i]};  protected: -inf
+ * plus the optional per-step statistics (see stepkv_score). No workspace.
+ * Errors: EINVAL, EUNSUPPORTED (pool window, stats step count), EHIP. */
+int stepkv_priority(const stepkv_problem* pb, const stepkv_params* prm, const float* saliency,
+                    const int32_t* step_ids, const uint8_t* protected_mask,
+                    const float* step_utility, float* scores, stepkv_step_stat* step_stats,
+                    void* stream);
+
+/* Sec. 5.2: token saliency and retention priority, for every (layer, KV head).
+ * For each sequence s, layer l and KV head h, with window rows r = w*G + g
+ * (query head h*G + g) and the N_s keys of s:
+ *   A_i   = sum_r softmax_i(scale * q_r . k_i)      (all N_s keys visible)
+ *   T_i   = (1/k) sum_{|j-i| <= k/2} A_j [j prunable], zero padding, per sequence
+ *   Th_i  = T_i / max_{prunable} T  (0 when that max is 0)
+ *   P_i   = alpha * Th_i + beta * S_{step_ids[i]}   (eq. token-priority)
+ * Protected tokens get P = -inf. A step id outside [0, n_steps_s) contributes
+ * utility 0 and is left out of step_stats.
+ * Outputs: scores (required); saliency = A (optional, NULL to skip);
+ * step_stats [L][Hkv][cu_steps[S]] (optional, NULL to skip).
+ * Errors: EINVAL for null required pointers or a bad problem/params,
+ * EUNSUPPORTED for d not in {64,128}, W*G > STEPKV_MAX_WINDOW_ROWS or a
+ * pool window above STEPKV_MAX_POOL_KERNEL (or more than
+ * STEPKV_MAX_STEPS_STATS steps in one sequence when step_stats is requested),
+ * EWORKSPACE when ws_bytes < stepkv_score_workspace_bytes(pb), EHIP on launch
+ * failure. Results are deterministic (fixed reduction orders). */
+int stepkv_score(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                 const void* k, const int32_t* step_ids, const uint8_t* protected_mask,
+                 const float* step_utility, float* scores, float* saliency,
+                 stepkv_step_stat* step_stats, void* workspace, size_t ws_bytes, void* stream);
+
+/* Sec. 5.2 / Algorithm 1 phase 3 / eq. problem: for every (sequence, layer,
+ * KV head), keep every protected token plus exactly min(B, N_pr) prunable
+ * tokens, the first in the order (score descending, position ascending),
+ * where NaN scores rank as -inf and -0.0 as +0.0. B is `budget`, or
+ * budgets[s] when `budgets` (device int32 [S]) is non-NULL.
+ * Writes idx (positions local to the sequence, ascending), cu_retained
+ * (R_s = n_protected_s + min(B_s, N_pr_s) prefix-summed) and, optionally,
+ * kept_per_step int32 [L][Hkv][cu_steps[S]] (retained prunable tokens per step).
+ * Errors: EINVAL for null required pointers, a bad problem, budget < 1 (when
+ * budgets is NULL); EHIP on launch failure. Budgets below 1 in `budgets` are
+ * treated as 1. Deterministic. */
+int stepkv_select(const stepkv_problem* pb, const float* scores, const uint8_t* protected_mask,
+                  const int32_t* step_ids, int32_t budget, const int32_t* budgets, int32_t* idx,
+                  int32_t* cu_retained, int32_t* kept_per_step, void* stream);
+
+/* eq. problem: C_hat = C_prot || C_traj[K]. For every (l, h) and sequence s,
+ * k_out[l][h][cu_retained[s] + j] = k[l][h][cu_seqlens[s] + idx[l][h][cu_seqlens[s] + j]]
+ * for j < R_s, and likewise v. Rows at or beyond out_rows are not written
+ * (cu_retained[S] gives the rows needed). A bit-exact copy; the outputs must
+ * not overlap the inputs. Errors: EINVAL for null pointers, a bad problem or
+ * out_rows < 0; EHIP on launch failure. */
+int stepkv_compact(const stepkv_problem* pb, const void* k, const void* v, const int32_t* idx,
+                   const int32_t* cu_retained, int32_t out_rows, void* k_out, void* v_out,
+                   void* stream);
+
+/* One decode step over a compacted cache, to check that the compacted cache
+ * is usable: for every layer l, sequence s and query head hq (KV head
+ * hq / G), out = softmax(scale * q . K_hat^T) V_hat over the R_s rows of s.
+ * q_dec bf16 [L][S][Hq][d]; out fp32 [L][S][Hq][d]; scale <= 0 selects
+ * 1/sqrt(d). Errors: EINVAL, EUNSUPPORTED (d), EHIP. */
+int stepkv_decode_attention(const stepkv_problem* pb, const void* q_dec, const void* k_hat,
+                            const void* v_hat, const int32_t* cu_retained, int32_t out_rows,
+                            float scale, float* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STEPKV_H_ */

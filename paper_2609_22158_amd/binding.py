@@ -1,0 +1,433 @@
+"""ctypes binding of libstepkv.so (the C ABI declared in include/stepkv.h).
+
+Argument marshalling only: every step of the compression pass runs in the
+library's HIP kernels. PyTorch supplies device memory and the current stream.
+There is no CPU fallback; a missing library raises at load time.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstepkv.so")
+
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
+MAX_WINDOW_ROWS = 256
+MAX_POOL_KERNEL = 63
+MAX_STEPS_STATS = 4096
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_f32p = ctypes.POINTER(ctypes.c_float)
+_f64p = ctypes.POINTER(ctypes.c_double)
+_vp = ctypes.c_void_p
+
+
+class ProblemC(ctypes.Structure):
+    _fields_ = [
+        ("num_layers", ctypes.c_int32),
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("window", ctypes.c_int32),
+        ("num_seqs", ctypes.c_int32),
+        ("cu_seqlens_host", _i32p),
+        ("cu_seqlens", _vp),
+        ("cu_steps_host", _i32p),
+        ("cu_steps", _vp),
+    ]
+
+
+class ParamsC(ctypes.Structure):
+    _fields_ = [
+        ("alpha", ctypes.c_float),
+        ("beta", ctypes.c_float),
+        ("pool_kernel", ctypes.c_int32),
+        ("scale", ctypes.c_float),
+        ("lambda_red", ctypes.c_float),
+        ("w_r", ctypes.c_float),
+        ("w_c", ctypes.c_float),
+        ("r_min", ctypes.c_float),
+        ("r_max", ctypes.c_float),
+        ("s_max", ctypes.c_float),
+        ("eta", ctypes.c_float),
+    ]
+
+
+class StepStatC(ctypes.Structure):
+    _fields_ = [
+        ("count", ctypes.c_uint32),
+        ("max_saliency", ctypes.c_float),
+        ("sum_saliency_q32", ctypes.c_uint64),
+    ]
+
+
+class StepStateC(ctypes.Structure):
+    _fields_ = [
+        ("capacity", ctypes.c_int32),
+        ("num_steps", ctypes.c_int32),
+        ("r", _f64p),
+        ("c", _f64p),
+    ]
+
+
+_SIGNATURES = {
+    "stepkv_params_default": (None, [ctypes.POINTER(ParamsC)]),
+    "stepkv_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "stepkv_budget_from_ratio": (ctypes.c_int64, [ctypes.c_double, ctypes.c_int64]),
+    "stepkv_step_update": (ctypes.c_int, [ctypes.POINTER(StepStateC), ctypes.c_float,
+                                          ctypes.c_float, ctypes.c_float, _f32p,
+                                          ctypes.POINTER(ParamsC), _f32p]),
+    "stepkv_score_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
+    "stepkv_saliency_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
+    "stepkv_saliency": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp,
+                                       _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "stepkv_priority": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp,
+                                       _vp, _vp, _vp, _vp, _vp, _vp]),
+    "stepkv_score": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp, _vp,
+                                    _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "stepkv_select": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, _vp, _vp, ctypes.c_int32,
+                                     _vp, _vp, _vp, _vp, _vp]),
+    "stepkv_compact": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, _vp, _vp, _vp,
+                                      ctypes.c_int32, _vp, _vp, _vp]),
+    "stepkv_decode_attention": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, _vp, _vp, _vp,
+                                               ctypes.c_int32, ctypes.c_float, _vp, _vp]),
+}
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+class StepKVError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__(f"{fn} failed: {code} ({strerror(code)})")
+        self.code = code
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libstepkv.so and declare its signatures; raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(
+            f"{path} not found: build it with `python -m paper_2609_22158_amd.build` "
+            "(hipcc, gfx950); there is no fallback implementation")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def strerror(code: int) -> str:
+    return load().stepkv_strerror(code).decode()
+
+
+def _check(fn: str, rc: int) -> None:
+    if rc != OK:
+        raise StepKVError(fn, rc)
+
+
+# ---------------------------------------------------------------- parameters
+@dataclass
+class Params:
+    """Method parameters; defaults are the paper's (filled by the library)."""
+
+    alpha: float = 0.2
+    beta: float = 0.8
+    pool_kernel: int = 7
+    scale: float = 0.0  # <= 0: 1/sqrt(d)
+    lambda_red: float = 0.3
+    w_r: float = 0.85
+    w_c: float = 0.15
+    r_min: float = -1.0
+    r_max: float = 2.0
+    s_max: float = 8.0
+    eta: float = 1.5
+
+    def c(self) -> ParamsC:
+        return ParamsC(*[getattr(self, f) for f, _ in ParamsC._fields_])
+
+    @staticmethod
+    def library_default() -> "Params":
+        p = ParamsC()
+        load().stepkv_params_default(ctypes.byref(p))
+        return Params(**{f: getattr(p, f) for f, _ in ParamsC._fields_})
+
+
+def budget_from_ratio(rho: float, n_prunable: int) -> int:
+    return int(load().stepkv_budget_from_ratio(float(rho), int(n_prunable)))
+
+
+def step_utilities(valid: Sequence[float], gain: Sequence[float], red: Sequence[float],
+                   obs_sim: np.ndarray, params: Optional[Params] = None) -> np.ndarray:
+    """Run the host step-utility update over boundaries 1..n; returns S (float32 [n])."""
+    lib = load()
+    p = (params or Params()).c()
+    n = len(valid)
+    r = np.zeros(max(n, 1), np.float64)
+    c = np.zeros(max(n, 1), np.float64)
+    st = StepStateC(max(n, 1), 0, r.ctypes.data_as(_f64p), c.ctypes.data_as(_f64p))
+    S = np.zeros(max(n, 1), np.float32)
+    sim = np.ascontiguousarray(obs_sim, dtype=np.float32)
+    for t in range(n):
+        row = np.ascontiguousarray(sim[t, :t]) if t > 0 else None
+        rc = lib.stepkv_step_update(ctypes.byref(st), float(valid[t]), float(gain[t]),
+                                    float(red[t]),
+                                    row.ctypes.data_as(_f32p) if row is not None else None,
+                                    ctypes.byref(p), S.ctypes.data_as(_f32p))
+        _check("stepkv_step_update", rc)
+    return S[:n].copy()
+
+
+# ---------------------------------------------------------------- problem
+class Problem:
+    """Shape of one compression problem with host and device offset arrays."""
+
+    def __init__(self, num_layers: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                 window: int, cu_seqlens, cu_steps, device="cuda"):
+        import torch
+
+        self.cu_seqlens = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+        self.cu_steps = np.ascontiguousarray(cu_steps, dtype=np.int32)
+        self.num_seqs = int(self.cu_seqlens.shape[0] - 1)
+        self.cu_seqlens_dev = torch.from_numpy(self.cu_seqlens).to(device)
+        self.cu_steps_dev = torch.from_numpy(self.cu_steps).to(device)
+        self.num_layers, self.num_q_heads, self.num_kv_heads = num_layers, num_q_heads, num_kv_heads
+        self.head_dim, self.window = head_dim, window
+        self.device = device
+        self.c = ProblemC(num_layers, num_q_heads, num_kv_heads, head_dim, window, self.num_seqs,
+                          self.cu_seqlens.ctypes.data_as(_i32p), self.cu_seqlens_dev.data_ptr(),
+                          self.cu_steps.ctypes.data_as(_i32p), self.cu_steps_dev.data_ptr())
+
+    @classmethod
+    def from_workload(cls, w, device="cuda") -> "Problem":
+        return cls(w.num_layers, w.num_q_heads, w.num_kv_heads, w.head_dim, w.window,
+                   w.cu_seqlens, w.cu_steps, device)
+
+    @property
+    def ntot(self) -> int:
+        return int(self.cu_seqlens[-1])
+
+    @property
+    def total_steps(self) -> int:
+        return int(self.cu_steps[-1])
+
+    @property
+    def lh(self) -> int:
+        return self.num_layers * self.num_kv_heads
+
+    def workspace_bytes(self) -> int:
+        return int(load().stepkv_score_workspace_bytes(ctypes.byref(self.c)))
+
+    def saliency_workspace_bytes(self) -> int:
+        return int(load().stepkv_saliency_workspace_bytes(ctypes.byref(self.c)))
+
+
+def _stream(stream) -> int:
+    import torch
+
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def _need(t, dtype, shape, name):
+    import torch
+
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous() or t.device.type != "cuda":
+        raise ValueError(f"{name}: must be a contiguous CUDA tensor")
+    return t.data_ptr()
+
+
+def score(pb: Problem, q_win, k, step_ids, protected, step_utility, params: Optional[Params] = None,
+          *, want_saliency: bool = False, want_stats: bool = False, workspace=None, scores=None,
+          stream=None):
+    """stepkv_score: priorities P [L*Hkv][Ntot] (and optionally A and step stats)."""
+    import torch
+
+    lib = load()
+    L, Hkv, d, W, S = pb.num_layers, pb.num_kv_heads, pb.head_dim, pb.window, pb.num_seqs
+    dev = pb.device
+    qp = _need(q_win, torch.bfloat16, (L, S, W, pb.num_q_heads, d), "q_win")
+    kp = _need(k, torch.bfloat16, (L, Hkv, pb.ntot, d), "k")
+    sp = _need(step_ids, torch.int32, (pb.ntot,), "step_ids")
+    pp = _need(protected, torch.uint8, (pb.ntot,), "protected")
+    up = _need(step_utility, torch.float32, (pb.total_steps,), "step_utility")
+    if scores is None:
+        scores = torch.empty((L, Hkv, pb.ntot), dtype=torch.float32, device=dev)
+    out = {"scores": scores}
+    sal = torch.empty((L, Hkv, pb.ntot), dtype=torch.float32, device=dev) if want_saliency else None
+    stats = (torch.empty((L, Hkv, pb.total_steps, 2), dtype=torch.int64, device=dev)
+             if want_stats else None)
+    need = pb.workspace_bytes()
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lib.stepkv_score(ctypes.byref(pb.c), ctypes.byref((params or Params()).c()), qp, kp, sp, pp,
+                          up, scores.data_ptr(), sal.data_ptr() if sal is not None else None,
+                          stats.data_ptr() if stats is not None else None, workspace.data_ptr(),
+                          workspace.numel(), _stream(stream))
+    _check("stepkv_score", rc)
+    if sal is not None:
+        out["saliency"] = sal
+    if stats is not None:
+        out["stats_raw"] = stats
+    return out
+
+
+def saliency(pb: Problem, q_win, k, params: Optional[Params] = None, *, workspace=None, out=None,
+             stream=None):
+    """stepkv_saliency: raw window saliency A [L][Hkv][Ntot] (fp32)."""
+    import torch
+
+    lib = load()
+    L, Hkv, d, W, S = pb.num_layers, pb.num_kv_heads, pb.head_dim, pb.window, pb.num_seqs
+    qp = _need(q_win, torch.bfloat16, (L, S, W, pb.num_q_heads, d), "q_win")
+    kp = _need(k, torch.bfloat16, (L, Hkv, pb.ntot, d), "k")
+    if out is None:
+        out = torch.empty((L, Hkv, pb.ntot), dtype=torch.float32, device=pb.device)
+    _need(out, torch.float32, (L, Hkv, pb.ntot), "saliency")
+    if workspace is None:
+        workspace = torch.empty(max(pb.saliency_workspace_bytes(), 1), dtype=torch.uint8,
+                                device=pb.device)
+    rc = lib.stepkv_saliency(ctypes.byref(pb.c), ctypes.byref((params or Params()).c()), qp, kp,
+                             out.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                             _stream(stream))
+    _check("stepkv_saliency", rc)
+    return out
+
+
+def priority(pb: Problem, sal, step_ids, protected, step_utility,
+             params: Optional[Params] = None, *, want_stats: bool = False, scores=None,
+             stream=None):
+    """stepkv_priority: P [L][Hkv][Ntot] from a saliency (and optionally step stats)."""
+    import torch
+
+    lib = load()
+    L, Hkv = pb.num_layers, pb.num_kv_heads
+    ap = _need(sal, torch.float32, (L, Hkv, pb.ntot), "saliency")
+    sp = _need(step_ids, torch.int32, (pb.ntot,), "step_ids")
+    pp = _need(protected, torch.uint8, (pb.ntot,), "protected")
+    up = _need(step_utility, torch.float32, (pb.total_steps,), "step_utility")
+    if scores is None:
+        scores = torch.empty((L, Hkv, pb.ntot), dtype=torch.float32, device=pb.device)
+    _need(scores, torch.float32, (L, Hkv, pb.ntot), "scores")
+    stats = (torch.empty((L, Hkv, pb.total_steps, 2), dtype=torch.int64, device=pb.device)
+             if want_stats else None)
+    rc = lib.stepkv_priority(ctypes.byref(pb.c), ctypes.byref((params or Params()).c()), ap, sp,
+                             pp, up, scores.data_ptr(),
+                             stats.data_ptr() if stats is not None else None, _stream(stream))
+    _check("stepkv_priority", rc)
+    out = {"scores": scores}
+    if stats is not None:
+        out["stats_raw"] = stats
+    return out
+
+
+def decode_stats(stats_raw) -> dict:
+    """Split the packed stepkv_step_stat records into count / max / sum arrays (host)."""
+    raw = stats_raw.cpu().numpy().reshape(-1, 2)
+    lo = raw[:, 0].view(np.uint64)
+    count = (lo & np.uint64(0xFFFFFFFF)).astype(np.int64)
+    mx = (lo >> np.uint64(32)).astype(np.uint32).view(np.float32)
+    sm = raw[:, 1].view(np.uint64).astype(np.float64) / 2.0**32
+    shape = stats_raw.shape[:-1]
+    return {"count": count.reshape(shape), "max": mx.reshape(shape), "sum": sm.reshape(shape)}
+
+
+def select(pb: Problem, scores, protected, step_ids, budget: int, *, budgets=None,
+           want_kept: bool = False, idx=None, cu_retained=None, stream=None):
+    """stepkv_select: idx [L][Hkv][Ntot] (sequence s at cu_seqlens[s]) and cu_retained [S+1]."""
+    import torch
+
+    lib = load()
+    L, Hkv, dev = pb.num_layers, pb.num_kv_heads, pb.device
+    scp = _need(scores, torch.float32, (L, Hkv, pb.ntot), "scores")
+    pp = _need(protected, torch.uint8, (pb.ntot,), "protected")
+    sp = _need(step_ids, torch.int32, (pb.ntot,), "step_ids")
+    bp = _need(budgets, torch.int32, (pb.num_seqs,), "budgets") if budgets is not None else None
+    if idx is None:
+        idx = torch.empty((L, Hkv, pb.ntot), dtype=torch.int32, device=dev)
+    _need(idx, torch.int32, (L, Hkv, pb.ntot), "idx")
+    cu_ret = cu_retained
+    if cu_ret is None:
+        cu_ret = torch.empty(pb.num_seqs + 1, dtype=torch.int32, device=dev)
+    _need(cu_ret, torch.int32, (pb.num_seqs + 1,), "cu_retained")
+    kept = torch.empty((L, Hkv, pb.total_steps), dtype=torch.int32, device=dev) if want_kept else None
+    rc = lib.stepkv_select(ctypes.byref(pb.c), scp, pp, sp, int(budget), bp, idx.data_ptr(),
+                           cu_ret.data_ptr(), kept.data_ptr() if kept is not None else None,
+                           _stream(stream))
+    _check("stepkv_select", rc)
+    return idx, cu_ret, kept
+
+
+def compact(pb: Problem, k, v, idx, cu_retained, out_rows: int, *, k_out=None, v_out=None,
+            stream=None):
+    """stepkv_compact: dense retained cache [L][Hkv][out_rows][d] for K and V."""
+    import torch
+
+    lib = load()
+    L, Hkv, d, dev = pb.num_layers, pb.num_kv_heads, pb.head_dim, pb.device
+    kp = _need(k, torch.bfloat16, (L, Hkv, pb.ntot, d), "k")
+    vp = _need(v, torch.bfloat16, (L, Hkv, pb.ntot, d), "v")
+    ip = _need(idx, torch.int32, (L, Hkv, pb.ntot), "idx")
+    cp = _need(cu_retained, torch.int32, (pb.num_seqs + 1,), "cu_retained")
+    if k_out is None:
+        k_out = torch.empty((L, Hkv, out_rows, d), dtype=torch.bfloat16, device=dev)
+    if v_out is None:
+        v_out = torch.empty((L, Hkv, out_rows, d), dtype=torch.bfloat16, device=dev)
+    _need(k_out, torch.bfloat16, (L, Hkv, out_rows, d), "k_out")
+    _need(v_out, torch.bfloat16, (L, Hkv, out_rows, d), "v_out")
+    rc = lib.stepkv_compact(ctypes.byref(pb.c), kp, vp, ip, cp, int(out_rows), k_out.data_ptr(),
+                            v_out.data_ptr(), _stream(stream))
+    _check("stepkv_compact", rc)
+    return k_out, v_out
+
+
+def decode_attention(pb: Problem, q_dec, k_hat, v_hat, cu_retained, out_rows: int,
+                     scale: float = 0.0, stream=None):
+    """stepkv_decode_attention: fp32 [L][S][Hq][d]."""
+    import torch
+
+    lib = load()
+    L, S, Hq, Hkv, d = pb.num_layers, pb.num_seqs, pb.num_q_heads, pb.num_kv_heads, pb.head_dim
+    qp = _need(q_dec, torch.bfloat16, (L, S, Hq, d), "q_dec")
+    kp = _need(k_hat, torch.bfloat16, (L, Hkv, out_rows, d), "k_hat")
+    vp = _need(v_hat, torch.bfloat16, (L, Hkv, out_rows, d), "v_hat")
+    cp = _need(cu_retained, torch.int32, (S + 1,), "cu_retained")
+    out = torch.empty((L, S, Hq, d), dtype=torch.float32, device=pb.device)
+    rc = lib.stepkv_decode_attention(ctypes.byref(pb.c), qp, kp, vp, cp, int(out_rows),
+                                     float(scale), out.data_ptr(), _stream(stream))
+    _check("stepkv_decode_attention", rc)
+    return out
+
+
+def retained_rows(seqlens: Sequence[int], protected_counts: Sequence[int], budget: int) -> int:
+    """Rows per (layer, head) of the compacted cache: sum of P_s + min(B, N_s - P_s)."""
+    return int(sum(p + min(budget, n - p) for n, p in zip(seqlens, protected_counts)))
+
+
+def compress(pb: Problem, q_win, k, v, step_ids, protected, step_utility, budget: int,
+             out_rows: int, params: Optional[Params] = None, stream=None):
+    """score -> select -> compact on one stream."""
+    sc = score(pb, q_win, k, step_ids, protected, step_utility, params, stream=stream)
+    idx, cu_ret, _ = select(pb, sc["scores"], protected, step_ids, budget, stream=stream)
+    k_hat, v_hat = compact(pb, k, v, idx, cu_ret, out_rows, stream=stream)
+    return {"scores": sc["scores"], "idx": idx, "cu_retained": cu_ret, "k_hat": k_hat,
+            "v_hat": v_hat}
+
+
+def bf16_from_bits(bits: np.ndarray, device="cuda"):
+    """Move bf16 bit patterns (uint16 numpy) to a torch bfloat16 tensor on `device`."""
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(device).view(
+        torch.bfloat16)

@@ -1,0 +1,397 @@
+// C ABI of the StepKV compression pass: argument validation, launch planning,
+// workspace layout, and the host-side step-utility update (Algorithm 1
+// phases 1-2). Every device computation is a kernel launched from here.
+#include "stepkv.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <limits>
+
+#include "internal.h"
+
+using namespace stepkv;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kMinItems = 2048;  // saliency work items wanted: ~8 per CU on 256 CUs
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool monotone_from_zero(const int32_t* cu, int n) {
+  if (cu[0] != 0) return false;
+  for (int i = 0; i < n; ++i)
+    if (cu[i + 1] < cu[i]) return false;
+  return true;
+}
+
+int check_problem(const stepkv_problem* pb) {
+  if (!pb) return STEPKV_EINVAL;
+  if (pb->num_layers < 1 || pb->num_q_heads < 1 || pb->num_kv_heads < 1 || pb->window < 1 ||
+      pb->num_seqs < 1 || pb->head_dim < 1)
+    return STEPKV_EINVAL;
+  if (pb->num_q_heads % pb->num_kv_heads != 0) return STEPKV_EINVAL;
+  if (!pb->cu_seqlens_host || !pb->cu_seqlens || !pb->cu_steps_host || !pb->cu_steps)
+    return STEPKV_EINVAL;
+  if (!monotone_from_zero(pb->cu_seqlens_host, pb->num_seqs)) return STEPKV_EINVAL;
+  if (!monotone_from_zero(pb->cu_steps_host, pb->num_seqs)) return STEPKV_EINVAL;
+  if (pb->head_dim != 64 && pb->head_dim != 128) return STEPKV_EUNSUPPORTED;
+  const int64_t lh = (int64_t)pb->num_layers * pb->num_kv_heads;
+  if (lh * pb->num_seqs > std::numeric_limits<int32_t>::max()) return STEPKV_EUNSUPPORTED;
+  return STEPKV_OK;
+}
+
+int window_rows(const stepkv_problem* pb) {
+  return (int)std::min<int64_t>((int64_t)pb->window * (pb->num_q_heads / pb->num_kv_heads),
+                                std::numeric_limits<int32_t>::max());
+}
+
+int max_seqlen(const stepkv_problem* pb) {
+  int m = 0;
+  for (int s = 0; s < pb->num_seqs; ++s)
+    m = std::max(m, pb->cu_seqlens_host[s + 1] - pb->cu_seqlens_host[s]);
+  return m;
+}
+
+struct SaliencyPlan {
+  int R, rows_pad, chunk, total_chunks;
+};
+
+SaliencyPlan plan_saliency(const stepkv_problem* pb) {
+  SaliencyPlan p;
+  p.R = window_rows(pb);
+  p.rows_pad = saliency_rows_pad(p.R);
+  const int64_t lh = (int64_t)pb->num_layers * pb->num_kv_heads;
+  auto chunks_for = [&](int c) {
+    int64_t t = 0;
+    for (int s = 0; s < pb->num_seqs; ++s)
+      t += (pb->cu_seqlens_host[s + 1] - pb->cu_seqlens_host[s] + c - 1) / c;
+    return t;
+  };
+  // largest chunk that still gives enough workgroups; all are multiples of
+  // every key tile (32, 64, 128)
+  p.chunk = 256;
+  for (int c : {4096, 2048, 1024, 512}) {
+    if (lh * chunks_for(c) >= kMinItems) {
+      p.chunk = c;
+      break;
+    }
+  }
+  p.total_chunks = (int)chunks_for(p.chunk);
+  return p;
+}
+
+struct WsLayout {
+  size_t cu_chunks, partial, lse, sal, total;
+};
+
+WsLayout layout(const stepkv_problem* pb, const SaliencyPlan& p) {
+  const size_t lh = (size_t)pb->num_layers * pb->num_kv_heads;
+  const size_t ntot = (size_t)pb->cu_seqlens_host[pb->num_seqs];
+  WsLayout w;
+  size_t off = 0;
+  w.cu_chunks = off;
+  off = align_up(off + sizeof(int32_t) * (pb->num_seqs + 1));
+  w.partial = off;
+  off = align_up(off + sizeof(float) * 2 * lh * p.total_chunks * p.rows_pad);
+  w.lse = off;
+  off = align_up(off + sizeof(float) * pb->num_seqs * lh * p.rows_pad);
+  w.sal = off;
+  off = align_up(off + sizeof(float) * lh * ntot);
+  w.total = off;
+  return w;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? STEPKV_OK : STEPKV_EHIP; }
+
+double utility(double r, double c, const stepkv_params* p) {
+  const double inner = std::min<double>(std::max<double>(r, p->r_min), p->r_max);
+  const double v = (double)p->w_r * inner + (double)p->w_c * std::log1p(c);
+  return std::min<double>(std::max(v, 0.0), p->s_max);
+}
+
+}  // namespace
+
+extern "C" {
+
+void stepkv_params_default(stepkv_params* p) {
+  if (!p) return;
+  p->alpha = 0.2f;
+  p->beta = 0.8f;
+  p->pool_kernel = 7;
+  p->scale = 0.0f;
+  p->lambda_red = 0.3f;
+  p->w_r = 0.85f;
+  p->w_c = 0.15f;
+  p->r_min = -1.0f;
+  p->r_max = 2.0f;
+  p->s_max = 8.0f;
+  p->eta = 1.5f;
+}
+
+const char* stepkv_strerror(int code) {
+  switch (code) {
+    case STEPKV_OK: return "ok";
+    case STEPKV_EINVAL: return "invalid argument";
+    case STEPKV_EUNSUPPORTED: return "unsupported shape or parameter";
+    case STEPKV_EWORKSPACE: return "workspace missing or too small";
+    case STEPKV_EHIP: return "HIP launch or runtime error";
+    default: return "unknown error";
+  }
+}
+
+int64_t stepkv_budget_from_ratio(double rho, int64_t n_prunable) {
+  if (!(rho > 0.0 && rho <= 1.0) || n_prunable < 0) return -1;
+  const int64_t b = (int64_t)std::floor(rho * (double)n_prunable + 1e-9);
+  return std::max<int64_t>(1, b);
+}
+
+int stepkv_step_update(stepkv_step_state* st, float valid, float gain, float red,
+                       const float* obs_sim_prev, const stepkv_params* prm, float* S_out) {
+  if (!st || !prm || !S_out || !st->r || !st->c) return STEPKV_EINVAL;
+  const int t = st->num_steps;
+  if (t < 0 || t >= st->capacity) return STEPKV_EINVAL;
+  if (!std::isfinite(valid) || !std::isfinite(gain) || !std::isfinite(red)) return STEPKV_EINVAL;
+  if (t > 0 && !obs_sim_prev) return STEPKV_EINVAL;
+  for (int k = 0; k < t; ++k)
+    if (!(obs_sim_prev[k] >= 0.0f && obs_sim_prev[k] <= 1.0f)) return STEPKV_EINVAL;
+  // phase 1: new-step score (gain_1 = 1 and red_1 = 0 by definition)
+  const double g = t == 0 ? 1.0 : (double)gain;
+  const double rd = t == 0 ? 0.0 : (double)red;
+  st->r[t] = (double)valid + g - (double)prm->lambda_red * rd;
+  st->c[t] = 0.0;
+  // phase 2: reuse credit for every earlier step
+  for (int k = 0; k < t; ++k)
+    st->c[k] += std::min(1.0, (double)prm->eta * (double)obs_sim_prev[k]);
+  st->num_steps = t + 1;
+  for (int k = 0; k <= t; ++k) S_out[k] = (float)utility(st->r[k], st->c[k], prm);
+  return STEPKV_OK;
+}
+
+size_t stepkv_score_workspace_bytes(const stepkv_problem* pb) {
+  if (check_problem(pb) != STEPKV_OK) return 0;
+  return layout(pb, plan_saliency(pb)).total;
+}
+
+size_t stepkv_saliency_workspace_bytes(const stepkv_problem* pb) {
+  if (check_problem(pb) != STEPKV_OK) return 0;
+  return layout(pb, plan_saliency(pb)).sal;  // everything but the saliency buffer
+}
+
+}  // extern "C"
+
+namespace {
+
+int check_params(const stepkv_problem* pb, const stepkv_params* prm) {
+  if (!prm) return STEPKV_EINVAL;
+  if (!std::isfinite(prm->alpha) || !std::isfinite(prm->beta) || !std::isfinite(prm->scale))
+    return STEPKV_EINVAL;
+  if (prm->pool_kernel < 1 || prm->pool_kernel % 2 == 0) return STEPKV_EINVAL;
+  if (prm->pool_kernel > STEPKV_MAX_POOL_KERNEL) return STEPKV_EUNSUPPORTED;
+  if (window_rows(pb) > STEPKV_MAX_WINDOW_ROWS) return STEPKV_EUNSUPPORTED;
+  return STEPKV_OK;
+}
+
+int max_steps_per_seq(const stepkv_problem* pb) {
+  int m = 0;
+  for (int s = 0; s < pb->num_seqs; ++s)
+    m = std::max(m, pb->cu_steps_host[s + 1] - pb->cu_steps_host[s]);
+  return m;
+}
+
+// Saliency sweeps into `sal`, using workspace regions below layout().sal.
+int run_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                 const void* k, float* sal, uint8_t* ws, hipStream_t st) {
+  const SaliencyPlan plan = plan_saliency(pb);
+  const WsLayout w = layout(pb, plan);
+  const int d = pb->head_dim;
+  SaliencyArgs sa;
+  sa.q = static_cast<const uint16_t*>(q_win);
+  sa.k = static_cast<const uint16_t*>(k);
+  sa.cu_seqlens = pb->cu_seqlens;
+  sa.cu_chunks = reinterpret_cast<int32_t*>(ws + w.cu_chunks);
+  sa.partial = reinterpret_cast<float2*>(ws + w.partial);
+  sa.lse2 = reinterpret_cast<float*>(ws + w.lse);
+  sa.sal = sal;
+  sa.L = pb->num_layers;
+  sa.S = pb->num_seqs;
+  sa.W = pb->window;
+  sa.Hq = pb->num_q_heads;
+  sa.Hkv = pb->num_kv_heads;
+  sa.G = pb->num_q_heads / pb->num_kv_heads;
+  sa.R = plan.R;
+  sa.rows_pad = plan.rows_pad;
+  sa.ntot = pb->cu_seqlens_host[pb->num_seqs];
+  sa.chunk = plan.chunk;
+  sa.total_chunks = plan.total_chunks;
+  const double scale = prm->scale > 0.0f ? (double)prm->scale : 1.0 / std::sqrt((double)d);
+  sa.c = (float)(scale * 1.4426950408889634);  // log2(e)
+  return hip_status(launch_saliency(sa, d, st));
+}
+
+int run_priority(const stepkv_problem* pb, const stepkv_params* prm, const float* sal,
+                 const int32_t* step_ids, const uint8_t* protected_mask, const float* util,
+                 float* scores, stepkv_step_stat* stats, hipStream_t st) {
+  FuseArgs fa;
+  fa.sal = sal;
+  fa.cu_seqlens = pb->cu_seqlens;
+  fa.cu_steps = pb->cu_steps;
+  fa.step_ids = step_ids;
+  fa.prot = protected_mask;
+  fa.util = util;
+  fa.scores = scores;
+  fa.stats = stats;
+  fa.S = pb->num_seqs;
+  fa.LH = pb->num_layers * pb->num_kv_heads;
+  fa.ntot = pb->cu_seqlens_host[pb->num_seqs];
+  fa.total_steps = pb->cu_steps_host[pb->num_seqs];
+  fa.half = prm->pool_kernel / 2;
+  fa.max_steps = std::max(max_steps_per_seq(pb), 1);
+  fa.alpha = prm->alpha;
+  fa.beta = prm->beta;
+  return hip_status(launch_fuse(fa, st));
+}
+
+int check_priority_args(const stepkv_problem* pb, const int32_t* step_ids,
+                        const uint8_t* protected_mask, const float* util, const float* scores,
+                        const stepkv_step_stat* stats) {
+  if (!step_ids || !protected_mask || !scores) return STEPKV_EINVAL;
+  if (!util && pb->cu_steps_host[pb->num_seqs] > 0) return STEPKV_EINVAL;
+  if (stats && max_steps_per_seq(pb) > STEPKV_MAX_STEPS_STATS) return STEPKV_EUNSUPPORTED;
+  return STEPKV_OK;
+}
+
+bool aligned(const void* p) { return reinterpret_cast<uintptr_t>(p) % kAlign == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int stepkv_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                    const void* k, float* saliency, void* workspace, size_t ws_bytes,
+                    void* stream) {
+  int rc = check_problem(pb);
+  if (rc == STEPKV_OK) rc = check_params(pb, prm);
+  if (rc != STEPKV_OK) return rc;
+  if (!q_win || !k || !saliency) return STEPKV_EINVAL;
+  const WsLayout w = layout(pb, plan_saliency(pb));
+  if (!workspace || ws_bytes < w.sal || !aligned(workspace)) return STEPKV_EWORKSPACE;
+  if (pb->cu_seqlens_host[pb->num_seqs] == 0) return STEPKV_OK;
+  return run_saliency(pb, prm, q_win, k, saliency, static_cast<uint8_t*>(workspace),
+                      static_cast<hipStream_t>(stream));
+}
+
+int stepkv_priority(const stepkv_problem* pb, const stepkv_params* prm, const float* saliency,
+                    const int32_t* step_ids, const uint8_t* protected_mask,
+                    const float* step_utility, float* scores, stepkv_step_stat* step_stats,
+                    void* stream) {
+  int rc = check_problem(pb);
+  if (rc == STEPKV_OK) rc = check_params(pb, prm);
+  if (rc != STEPKV_OK) return rc;
+  if (!saliency) return STEPKV_EINVAL;
+  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats);
+  if (rc != STEPKV_OK) return rc;
+  if (pb->cu_seqlens_host[pb->num_seqs] == 0) return STEPKV_OK;
+  return run_priority(pb, prm, saliency, step_ids, protected_mask, step_utility, scores,
+                      step_stats, static_cast<hipStream_t>(stream));
+}
+
+int stepkv_score(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                 const void* k, const int32_t* step_ids, const uint8_t* protected_mask,
+                 const float* step_utility, float* scores, float* saliency,
+                 stepkv_step_stat* step_stats, void* workspace, size_t ws_bytes, void* stream) {
+  int rc = check_problem(pb);
+  if (rc == STEPKV_OK) rc = check_params(pb, prm);
+  if (rc != STEPKV_OK) return rc;
+  if (!q_win || !k) return STEPKV_EINVAL;
+  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats);
+  if (rc != STEPKV_OK) return rc;
+  const WsLayout w = layout(pb, plan_saliency(pb));
+  if (!workspace || ws_bytes < w.total || !aligned(workspace)) return STEPKV_EWORKSPACE;
+  if (pb->cu_seqlens_host[pb->num_seqs] == 0) return STEPKV_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  float* sal = saliency ? saliency : reinterpret_cast<float*>(ws + w.sal);
+  rc = run_saliency(pb, prm, q_win, k, sal, ws, st);
+  if (rc != STEPKV_OK) return rc;
+  return run_priority(pb, prm, sal, step_ids, protected_mask, step_utility, scores, step_stats,
+                      st);
+}
+
+int stepkv_select(const stepkv_problem* pb, const float* scores, const uint8_t* protected_mask,
+                  const int32_t* step_ids, int32_t budget, const int32_t* budgets, int32_t* idx,
+                  int32_t* cu_retained, int32_t* kept_per_step, void* stream) {
+  const int rc = check_problem(pb);
+  if (rc != STEPKV_OK) return rc;
+  if (!scores || !protected_mask || !idx || !cu_retained) return STEPKV_EINVAL;
+  if (kept_per_step && !step_ids) return STEPKV_EINVAL;
+  if (!budgets && budget < 1) return STEPKV_EINVAL;
+  SelectArgs a;
+  a.scores = scores;
+  a.prot = protected_mask;
+  a.step_ids = step_ids;
+  a.cu_seqlens = pb->cu_seqlens;
+  a.cu_steps = pb->cu_steps;
+  a.budgets = budgets;
+  a.idx = idx;
+  a.cu_retained = cu_retained;
+  a.kept = kept_per_step;
+  a.S = pb->num_seqs;
+  a.LH = pb->num_layers * pb->num_kv_heads;
+  a.ntot = pb->cu_seqlens_host[pb->num_seqs];
+  a.total_steps = pb->cu_steps_host[pb->num_seqs];
+  a.budget = std::max(budget, 1);
+  a.max_len = max_seqlen(pb);
+  return hip_status(launch_select(a, static_cast<hipStream_t>(stream)));
+}
+
+int stepkv_compact(const stepkv_problem* pb, const void* k, const void* v, const int32_t* idx,
+                   const int32_t* cu_retained, int32_t out_rows, void* k_out, void* v_out,
+                   void* stream) {
+  const int rc = check_problem(pb);
+  if (rc != STEPKV_OK) return rc;
+  if (!k || !v || !idx || !cu_retained || !k_out || !v_out || out_rows < 0) return STEPKV_EINVAL;
+  CompactArgs a;
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.idx = idx;
+  a.cu_seqlens = pb->cu_seqlens;
+  a.cu_retained = cu_retained;
+  a.k_out = static_cast<uint16_t*>(k_out);
+  a.v_out = static_cast<uint16_t*>(v_out);
+  a.S = pb->num_seqs;
+  a.LH = pb->num_layers * pb->num_kv_heads;
+  a.ntot = pb->cu_seqlens_host[pb->num_seqs];
+  a.out_rows = out_rows;
+  a.d = pb->head_dim;
+  return hip_status(launch_compact(a, static_cast<hipStream_t>(stream)));
+}
+
+int stepkv_decode_attention(const stepkv_problem* pb, const void* q_dec, const void* k_hat,
+                            const void* v_hat, const int32_t* cu_retained, int32_t out_rows,
+                            float scale, float* out, void* stream) {
+  const int rc = check_problem(pb);
+  if (rc != STEPKV_OK) return rc;
+  if (!q_dec || !k_hat || !v_hat || !cu_retained || !out || out_rows < 0 || !std::isfinite(scale))
+    return STEPKV_EINVAL;
+  DecodeArgs a;
+  a.q = static_cast<const uint16_t*>(q_dec);
+  a.k = static_cast<const uint16_t*>(k_hat);
+  a.v = static_cast<const uint16_t*>(v_hat);
+  a.cu_retained = cu_retained;
+  a.out = out;
+  a.L = pb->num_layers;
+  a.S = pb->num_seqs;
+  a.Hq = pb->num_q_heads;
+  a.Hkv = pb->num_kv_heads;
+  a.G = pb->num_q_heads / pb->num_kv_heads;
+  a.d = pb->head_dim;
+  a.out_rows = out_rows;
+  a.scale = scale > 0.0f ? scale : (float)(1.0 / std::sqrt((double)pb->head_dim));
+  return hip_status(launch_decode(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+// Kernel launch interface between the C ABI layer (api.cpp) and the HIP
+// kernels. Every launcher enqueues on the given stream and returns the
+// hipError_t of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace stepkv {
+
+// ---------------------------------------------------------------- saliency
+struct SaliencyArgs {
+  const uint16_t* q;         // bf16 [L][S][W][Hq][d]
+  const uint16_t* k;         // bf16 [L*Hkv][Ntot][d]
+  const int32_t* cu_seqlens; // [S+1]
+  int32_t* cu_chunks;        // [S+1] chunk prefix (written by the plan kernel)
+  float2* partial;           // [L*Hkv][total_chunks][rows_pad] (log2 max, sum)
+  float* lse2;               // [S][L*Hkv][rows_pad] log2-domain log-sum-exp
+  float* sal;                // [L*Hkv][Ntot] A_i
+  int L, S, W, Hq, Hkv, G, R, rows_pad;
+  int ntot, chunk, total_chunks;
+  float c;  // softmax scale * log2(e)
+};
+
+// Rows padded to whole row groups: 64, 128 or 256.
+int saliency_rows_pad(int R);
+// Key tile processed per iteration by one workgroup.
+int saliency_tile_keys(int R);
+hipError_t launch_saliency(const SaliencyArgs& a, int d, hipStream_t st);
+
+// ---------------------------------------------------------------- fuse
+struct FuseArgs {
+  const float* sal;          // [L*Hkv][Ntot]
+  const int32_t* cu_seqlens; // [S+1]
+  const int32_t* cu_steps;   // [S+1]
+  const int32_t* step_ids;   // [Ntot]
+  const uint8_t* prot;       // [Ntot]
+  const float* util;         // [cu_steps[S]]
+  float* scores;             // [L*Hkv][Ntot]
+  void* stats;               // stepkv_step_stat [L*Hkv][cu_steps[S]] or null
+  int S, LH, ntot, total_steps, half, max_steps;
+  float alpha, beta;
+};
+hipError_t launch_fuse(const FuseArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- select
+struct SelectArgs {
+  const float* scores;       // [L*Hkv][Ntot]
+  const uint8_t* prot;       // [Ntot]
+  const int32_t* step_ids;   // [Ntot]
+  const int32_t* cu_seqlens; // [S+1]
+  const int32_t* cu_steps;   // [S+1]
+  const int32_t* budgets;    // [S] or null
+  int32_t* idx;              // [L*Hkv][Ntot]
+  int32_t* cu_retained;      // [S+1]
+  int32_t* kept;             // [L*Hkv][cu_steps[S]] or null
+  int S, LH, ntot, total_steps, budget, max_len;
+};
+hipError_t launch_select(const SelectArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- compact
+struct CompactArgs {
+  const uint16_t* k;         // bf16 [L*Hkv][Ntot][d]
+  const uint16_t* v;
+  const int32_t* idx;        // [L*Hkv][Ntot]
+  const int32_t* cu_seqlens; // [S+1]
+  const int32_t* cu_retained;// [S+1]
+  uint16_t* k_out;           // bf16 [L*Hkv][out_rows][d]
+  uint16_t* v_out;
+  int S, LH, ntot, out_rows, d;
+};
+hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- decode check
+struct DecodeArgs {
+  const uint16_t* q;         // bf16 [L][S][Hq][d]
+  const uint16_t* k;         // bf16 [L*Hkv][out_rows][d]
+  const uint16_t* v;
+  const int32_t* cu_retained;// [S+1]
+  float* out;                // [L][S][Hq][d]
+  int L, S, Hq, Hkv, G, d, out_rows;
+  float scale;
+};
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t st);
+
+}  // namespace stepkv

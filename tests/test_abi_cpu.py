@@ -1,0 +1,188 @@
+"""C ABI checks that need no GPU: exports, host helpers and argument validation.
+
+Validation runs on the host before any HIP call, so the device pointers below
+are never dereferenced (they are placeholders).
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2609_22158_amd import binding as B
+from synth import make_workload
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "stepkv.h")
+FAKE = 0x10000  # placeholder device address; never dereferenced by these calls
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return B.load()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(stepkv_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function(lib):
+    names = _declared_functions()
+    assert len(names) == 12, names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(B._SIGNATURES)
+
+
+def test_defaults_are_the_papers(lib):
+    p = B.Params.library_default()
+    assert (round(p.alpha, 6), round(p.beta, 6)) == (0.2, 0.8)
+    assert (round(p.lambda_red, 6), round(p.w_r, 6), round(p.w_c, 6)) == (0.3, 0.85, 0.15)
+    assert (p.r_min, p.r_max, p.s_max, p.eta, p.pool_kernel) == (-1.0, 2.0, 8.0, 1.5, 7)
+
+
+def test_strerror(lib):
+    assert B.strerror(0) == "ok"
+    assert "workspace" in B.strerror(-3)
+
+
+@pytest.mark.parametrize("rho,n", [(0.2, 1000), (0.2, 3), (0.29, 100), (0.5, 7), (1.0, 9), (0.3, 0)])
+def test_budget_from_ratio_matches_oracle(lib, rho, n):
+    assert B.budget_from_ratio(rho, n) == O.budget_from_ratio(rho, n)
+
+
+def test_budget_from_ratio_rejects(lib):
+    assert B.budget_from_ratio(0.0, 10) == -1
+    assert B.budget_from_ratio(1.5, 10) == -1
+    assert B.budget_from_ratio(0.5, -1) == -1
+
+
+@pytest.mark.parametrize("seed", [233, 42, 3407])
+def test_host_step_update_matches_oracle(lib, seed):
+    w = make_workload("l32_32k", seed, num_layers=1, with_v=False)
+    sig = w.signals[0]
+    S_c = B.step_utilities(sig.valid, sig.gain, sig.red, sig.obs_sim)
+    _, c_o, S_o = O.run_step_updates(sig.valid, sig.gain, sig.red,
+                                     sig.obs_sim.astype(np.float64), O.Params())
+    np.testing.assert_allclose(S_c, S_o, rtol=2e-7, atol=2e-7)
+    # planted steps are reused at every later boundary: min(1, 1.5 * sim) >= 0.75 each time
+    n = sig.num_steps
+    for k in w.planted_steps[0]:
+        assert c_o[k] >= 0.75 * (n - 1 - k) - 1e-9
+
+
+def test_host_step_update_rejects(lib):
+    p = B.Params().c()
+    r = np.zeros(2)
+    c = np.zeros(2)
+    st = B.StepStateC(2, 0, r.ctypes.data_as(B._f64p), c.ctypes.data_as(B._f64p))
+    S = np.zeros(2, np.float32)
+    Sp = S.ctypes.data_as(B._f32p)
+    assert lib.stepkv_step_update(ctypes.byref(st), 1, 1, 0, None, ctypes.byref(p), Sp) == 0
+    bad = np.array([1.5], np.float32)
+    assert lib.stepkv_step_update(ctypes.byref(st), 1, 1, 0, bad.ctypes.data_as(B._f32p),
+                                  ctypes.byref(p), Sp) == B.EINVAL
+    assert lib.stepkv_step_update(ctypes.byref(st), 1, 1, 0, None, ctypes.byref(p), Sp) == B.EINVAL
+    ok = np.array([0.5], np.float32)
+    assert lib.stepkv_step_update(ctypes.byref(st), 1, 0.5, 0, ok.ctypes.data_as(B._f32p),
+                                  ctypes.byref(p), Sp) == 0
+    assert lib.stepkv_step_update(ctypes.byref(st), 1, 1, 0, ok.ctypes.data_as(B._f32p),
+                                  ctypes.byref(p), Sp) == B.EINVAL  # capacity 2 reached
+    assert S[0] == pytest.approx(0.85 * 2 + 0.15 * np.log(1.75), abs=1e-6)
+
+
+def _problem(L=2, Hq=8, Hkv=2, d=128, W=32, cu=(0, 1000, 3000), cu_steps=(0, 4, 9)):
+    cu = np.array(cu, np.int32)
+    cs = np.array(cu_steps, np.int32)
+    pb = B.ProblemC(L, Hq, Hkv, d, W, len(cu) - 1, cu.ctypes.data_as(B._i32p), FAKE,
+                    cs.ctypes.data_as(B._i32p), FAKE)
+    pb._keep = (cu, cs)
+    return pb
+
+
+def _score(lib, pb, prm=None, ws_bytes=None, **ptrs):
+    prm = prm or B.Params().c()
+    args = dict(q=FAKE, k=FAKE, sid=FAKE, prot=FAKE, util=FAKE, scores=FAKE, sal=None, stats=None,
+                ws=FAKE * 16)
+    args.update(ptrs)
+    need = lib.stepkv_score_workspace_bytes(ctypes.byref(pb))
+    return lib.stepkv_score(ctypes.byref(pb), ctypes.byref(prm), args["q"], args["k"], args["sid"],
+                            args["prot"], args["util"], args["scores"], args["sal"],
+                            args["stats"], args["ws"], need if ws_bytes is None else ws_bytes,
+                            None)
+
+
+def test_workspace_bytes(lib):
+    pb = _problem()
+    n = lib.stepkv_score_workspace_bytes(ctypes.byref(pb))
+    # at least the fp32 saliency of every (layer, head, token)
+    assert n >= 4 * 2 * 2 * 3000 and n % 256 == 0
+    assert lib.stepkv_score_workspace_bytes(ctypes.byref(_problem(Hq=7))) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Hq=7), B.EINVAL),          # G not an integer
+    (dict(d=96), B.EUNSUPPORTED),    # head dim
+    (dict(d=0), B.EINVAL),
+    (dict(W=65, Hq=8, Hkv=2), B.EUNSUPPORTED),  # W*G = 260 > 256
+    (dict(cu=(0, 10, 5)), B.EINVAL),  # not monotone
+    (dict(cu=(1, 10, 20)), B.EINVAL),  # does not start at 0
+    (dict(L=0), B.EINVAL),
+])
+def test_score_rejects_problem(lib, kw, code):
+    assert _score(lib, _problem(**kw)) == code
+
+
+def test_score_rejects_arguments(lib):
+    pb = _problem()
+    assert _score(lib, pb, q=None) == B.EINVAL
+    assert _score(lib, pb, scores=None) == B.EINVAL
+    assert _score(lib, pb, util=None) == B.EINVAL
+    assert _score(lib, pb, ws=None) == B.EWORKSPACE
+    assert _score(lib, pb, ws_bytes=1024) == B.EWORKSPACE
+    assert _score(lib, pb, ws=FAKE * 16 + 8) == B.EWORKSPACE  # misaligned
+    assert _score(lib, pb, prm=B.Params(pool_kernel=6).c()) == B.EINVAL
+    assert _score(lib, pb, prm=B.Params(pool_kernel=65).c()) == B.EUNSUPPORTED
+    assert _score(lib, pb, prm=B.Params(alpha=float("nan")).c()) == B.EINVAL
+    many = _problem(cu_steps=(0, 4097, 4099))
+    assert _score(lib, many, stats=FAKE) == B.EUNSUPPORTED
+
+
+def test_saliency_priority_reject(lib):
+    pb = _problem()
+    prm = B.Params().c()
+    need = lib.stepkv_saliency_workspace_bytes(ctypes.byref(pb))
+    assert 0 < need < lib.stepkv_score_workspace_bytes(ctypes.byref(pb))
+    sal = lib.stepkv_saliency
+    assert sal(ctypes.byref(pb), ctypes.byref(prm), FAKE, FAKE, None, FAKE * 16, need,
+               None) == B.EINVAL
+    assert sal(ctypes.byref(pb), ctypes.byref(prm), FAKE, FAKE, FAKE, FAKE * 16, need - 256,
+               None) == B.EWORKSPACE
+    assert sal(ctypes.byref(_problem(W=128)), ctypes.byref(prm), FAKE, FAKE, FAKE, FAKE * 16,
+               need, None) == B.EUNSUPPORTED
+    pri = lib.stepkv_priority
+    assert pri(ctypes.byref(pb), ctypes.byref(prm), None, FAKE, FAKE, FAKE, FAKE, None,
+               None) == B.EINVAL
+    assert pri(ctypes.byref(pb), ctypes.byref(B.Params(pool_kernel=0).c()), FAKE, FAKE, FAKE,
+               FAKE, FAKE, None, None) == B.EINVAL
+
+
+def test_select_compact_decode_reject(lib):
+    pb = _problem()
+    assert lib.stepkv_select(ctypes.byref(pb), FAKE, FAKE, FAKE, 0, None, FAKE, FAKE, None,
+                             None) == B.EINVAL  # budget < 1
+    assert lib.stepkv_select(ctypes.byref(pb), None, FAKE, FAKE, 4, None, FAKE, FAKE, None,
+                             None) == B.EINVAL
+    assert lib.stepkv_select(ctypes.byref(pb), FAKE, FAKE, None, 4, None, FAKE, FAKE, FAKE,
+                             None) == B.EINVAL  # kept needs step ids
+    assert lib.stepkv_compact(ctypes.byref(pb), FAKE, FAKE, FAKE, FAKE, -1, FAKE, FAKE,
+                              None) == B.EINVAL
+    assert lib.stepkv_compact(ctypes.byref(pb), FAKE, None, FAKE, FAKE, 8, FAKE, FAKE,
+                              None) == B.EINVAL
+    assert lib.stepkv_decode_attention(ctypes.byref(_problem(d=80)), FAKE, FAKE, FAKE, FAKE, 8,
+                                       0.0, FAKE, None) == B.EUNSUPPORTED
+    assert lib.stepkv_decode_attention(ctypes.byref(pb), FAKE, FAKE, FAKE, FAKE, 8,
+                                       float("inf"), FAKE, None) == B.EINVAL

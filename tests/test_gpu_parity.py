@@ -1,0 +1,235 @@
+"""HIP path vs the CPU oracle, through the C ABI, on seeded synthetic caches.
+
+Scores and saliency: within 2e-3 relative (+1e-7 of the head's max).
+Selection: bit-exact when both sides rank the oracle's priorities cast to
+fp32; end to end, retained sets may differ only by tokens whose priority is
+tied with the threshold within that tolerance. Compaction: bit-exact.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+from tests.gpu_cases import (GpuRun, close, log, oracle_params, reduced, run_oracle, swap_ok)
+
+pytestmark = pytest.mark.gpu
+
+# sizes the oracle finishes in seconds, each spanning several key tiles and a
+# ragged tail, covering every window-row shape: W*G = 64, 128, 256, 224
+CASES = {
+    "tiny": dict(name="tiny"),  # the 1-layer, N=1024, d=64 configuration, unchanged
+    "l1_8k": dict(name="l1_8k"),  # the 8B-shaped single layer, N=8192, unchanged
+    "l1_tail3001": dict(name="l1_8k", seqlens=[3001]),
+    "l32_32k_2l": dict(name="l32_32k", num_layers=2, seqlens=[5003], num_steps=20),
+    "ragged_g7": dict(name="ragged16", num_layers=2, seqlens=[2500, 700, 130, 1, 0, 4097],
+                      protected_len=64),
+}
+
+_cache = {}
+
+
+def _case(cid):
+    if cid not in _cache:
+        spec = dict(CASES[cid])
+        name = spec.pop("name")
+        log(f"[case {cid}] generating")
+        w = reduced(name, **spec)
+        g = GpuRun(w)
+        log(f"[case {cid}] gpu score, L={w.num_layers} seqlens={w.seqlens} W={w.window} "
+            f"G={w.group} d={w.head_dim}")
+        sc = g.score(want_saliency=True, want_stats=True)
+        import torch
+
+        torch.cuda.synchronize()
+        log(f"[case {cid}] oracle")
+        o = run_oracle(w, g.budget, g.params)
+        _cache[cid] = (w, g, sc, o)
+    return _cache[cid]
+
+
+def _heads(w):
+    for s in range(w.num_seqs):
+        a, b = int(w.cu_seqlens[s]), int(w.cu_seqlens[s + 1])
+        for l in range(w.num_layers):
+            for h in range(w.num_kv_heads):
+                yield s, l, h, a, b
+
+
+@pytest.mark.parametrize("cid", list(CASES))
+def test_scores_and_saliency_match_oracle(cid):
+    w, g, sc, o = _case(cid)
+    P = sc["scores"].cpu().numpy()
+    A = sc["saliency"].cpu().numpy()
+    for s, l, h, a, b in _heads(w):
+        close(P[l, h, a:b], o["P"][(s, l, h)], f"P{(s, l, h)}")
+        close(A[l, h, a:b], o["A"][(s, l, h)], f"A{(s, l, h)}")
+        if b > a:
+            assert abs(A[l, h, a:b].sum() - w.window * w.group) < 1e-3 * w.window * w.group
+
+
+@pytest.mark.parametrize("cid", list(CASES))
+def test_step_statistics_match_oracle(cid):
+    from paper_2609_22158_amd import binding as B
+
+    w, g, sc, o = _case(cid)
+    st = B.decode_stats(sc["stats_raw"])
+    for s, l, h, a, b in _heads(w):
+        k0, k1 = int(w.cu_steps[s]), int(w.cu_steps[s + 1])
+        prun = w.protected[a:b] == 0
+        ref = O.step_statistics(o["T_hat"][(s, l, h)], w.step_ids[a:b], prun, k1 - k0)
+        assert np.array_equal(st["count"][l, h, k0:k1], ref["count"])
+        np.testing.assert_allclose(st["max"][l, h, k0:k1], ref["max"], rtol=2e-3, atol=1e-6)
+        np.testing.assert_allclose(st["sum"][l, h, k0:k1], ref["sum"], rtol=2e-3, atol=1e-4)
+
+
+def _oracle_scores_fp32(w, o):
+    import torch
+
+    P = np.full((w.num_layers, w.num_kv_heads, w.total_tokens), -np.inf, np.float32)
+    for s, l, h, a, b in _heads(w):
+        P[l, h, a:b] = o["P"][(s, l, h)].astype(np.float32)
+    return P, torch.from_numpy(P).cuda()
+
+
+def _check_selection(w, g, P32, idx, cu_ret, kept, heads=None):
+    """GPU selection on the oracle's fp32 priorities == oracle selection on the same numbers."""
+    rows = w.retained_rows(g.budget)
+    assert list(cu_ret) == list(np.concatenate([[0], np.cumsum(rows)]))
+    for s, l, h, a, b in _heads(w):
+        if heads is not None and (l, h) not in heads:
+            continue
+        prun = w.protected[a:b] == 0
+        ref = O.select_retained(P32[l, h, a:b], prun, g.budget)
+        got = idx[l, h, a:a + rows[s]]
+        assert np.array_equal(got, ref), f"idx{(s, l, h)}"
+        if kept is not None:
+            k0, k1 = int(w.cu_steps[s]), int(w.cu_steps[s + 1])
+            ref_k = O.kept_per_step(ref, w.step_ids[a:b], prun, k1 - k0)
+            assert np.array_equal(kept[l, h, k0:k1], ref_k), f"kept{(s, l, h)}"
+
+
+@pytest.mark.parametrize("cid", list(CASES))
+def test_select_and_compact_bitexact_on_oracle_scores(cid):
+    import torch
+
+    w, g, sc, o = _case(cid)
+    P32, Pdev = _oracle_scores_fp32(w, o)
+    log(f"[case {cid}] gpu select on oracle priorities")
+    idx, cu_ret, kept = g.select(Pdev, want_kept=True)
+    k_hat, v_hat = g.compact(idx, cu_ret)
+    torch.cuda.synchronize()
+    idx, cu_ret, kept = idx.cpu().numpy(), cu_ret.cpu().numpy(), kept.cpu().numpy()
+    _check_selection(w, g, P32, idx, cu_ret, kept)
+    kh = k_hat.view(torch.int16).cpu().numpy().view(np.uint16)
+    vh = v_hat.view(torch.int16).cpu().numpy().view(np.uint16)
+    rows = w.retained_rows(g.budget)
+    for s, l, h, a, b in _heads(w):
+        r0 = int(cu_ret[s])
+        sel = idx[l, h, a:a + rows[s]]
+        kr, vr = O.compact(w.k[l, h, a:b], w.v[l, h, a:b], sel)
+        assert np.array_equal(kh[l, h, r0:r0 + rows[s]], kr), f"k_hat{(s, l, h)}"
+        assert np.array_equal(vh[l, h, r0:r0 + rows[s]], vr), f"v_hat{(s, l, h)}"
+
+
+@pytest.mark.parametrize("cid", list(CASES))
+def test_end_to_end_selection_within_ties(cid):
+    w, g, sc, o = _case(cid)
+    log(f"[case {cid}] gpu select on gpu priorities")
+    idx, cu_ret, _ = g.select(sc["scores"])
+    idx = idx.cpu().numpy()
+    rows = w.retained_rows(g.budget)
+    for s, l, h, a, b in _heads(w):
+        got = idx[l, h, a:a + rows[s]]
+        assert (np.diff(got) > 0).all()
+        prun = w.protected[a:b] == 0
+        assert set(np.nonzero(~prun)[0]) <= set(got)
+        swap_ok(got, o["idx"][(s, l, h)], o["P"][(s, l, h)], prun, g.budget)
+
+
+@pytest.mark.parametrize("budget", [1, 7, 959, 960, 5000])
+def test_budget_edges(budget):
+    """B = 1, B one below and at N_pr = 960 (all kept), and B far above N_pr."""
+    import torch
+
+    w = reduced("tiny")
+    g = GpuRun(w, budget=budget)
+    log(f"[budget {budget}] gpu")
+    sc = g.score()
+    idx, cu_ret, kept = g.select(sc["scores"], want_kept=True)
+    torch.cuda.synchronize()
+    o = run_oracle(w, budget, g.params, want_saliency=False)
+    P32, Pdev = _oracle_scores_fp32(w, o)
+    idx2, cu2, kept2 = g.select(Pdev, want_kept=True)
+    _check_selection(w, g, P32, idx2.cpu().numpy(), cu2.cpu().numpy(), kept2.cpu().numpy())
+    n_keep = 64 + min(budget, 960)
+    assert int(cu_ret.cpu()[1]) == n_keep
+    idx = idx.cpu().numpy()
+    for s, l, h, a, b in _heads(w):
+        swap_ok(idx[l, h, :n_keep], o["idx"][(s, l, h)], o["P"][(s, l, h)],
+                w.protected == 0, budget)
+
+
+@pytest.mark.parametrize("alpha,beta", [(0.0, 0.8), (0.2, 0.0)])
+def test_single_signal_special_cases(alpha, beta):
+    """alpha = 0: whole steps by utility; beta = 0: pure pooled-saliency top-B (Table 3 ablations)."""
+    from paper_2609_22158_amd import binding as B
+
+    w = reduced("l1_8k", seqlens=[2049])
+    p = B.Params(alpha=alpha, beta=beta)
+    g = GpuRun(w, params=p)
+    log(f"[alpha {alpha} beta {beta}] gpu")
+    sc = g.score()
+    idx, _, _ = g.select(sc["scores"])
+    o = run_oracle(w, g.budget, p, want_saliency=False)
+    P = sc["scores"].cpu().numpy()
+    idx = idx.cpu().numpy()
+    rows = w.retained_rows(g.budget)
+    for s, l, h, a, b in _heads(w):
+        close(P[l, h, a:b], o["P"][(s, l, h)], f"P{(s, l, h)}")
+        prun = w.protected[a:b] == 0
+        swap_ok(idx[l, h, :rows[0]], o["idx"][(s, l, h)], o["P"][(s, l, h)], prun, g.budget)
+
+
+def test_repeat_runs_are_bitwise_identical():
+    import torch
+
+    w = reduced("l32_32k", num_layers=2, seqlens=[5003], num_steps=20)
+    g = GpuRun(w)
+    outs = []
+    for rep in range(3):
+        log(f"[determinism] run {rep}")
+        sc = g.score(want_saliency=True, want_stats=True)
+        idx, cu, kept = g.select(sc["scores"], want_kept=True)
+        k_hat, v_hat = g.compact(idx, cu)
+        torch.cuda.synchronize()
+        outs.append([t.cpu().numpy().tobytes() for t in
+                     (sc["scores"], sc["saliency"], sc["stats_raw"], idx, kept, k_hat.view(torch.int16))])
+    assert outs[0] == outs[1] == outs[2]
+
+
+def test_decode_over_compacted_cache():
+    """One decode step over the compacted ragged cache matches textbook attention."""
+    import torch
+
+    from paper_2609_22158_amd import binding as B
+
+    w = reduced("ragged16", num_layers=2, seqlens=[2500, 700, 130, 1, 4097], protected_len=64)
+    g = GpuRun(w)
+    o = run_oracle(w, g.budget, g.params, want_saliency=False)
+    P32, Pdev = _oracle_scores_fp32(w, o)
+    idx, cu_ret, _ = g.select(Pdev)
+    k_hat, v_hat = g.compact(idx, cu_ret)
+    qd = B.bf16_from_bits(w.q_dec)
+    log("[decode] gpu")
+    out = B.decode_attention(g.pb, qd, k_hat, v_hat, cu_ret, g.out_rows).cpu().numpy()
+    scale = 1.0 / np.sqrt(w.head_dim)
+    for s in range(w.num_seqs):
+        a, b = int(w.cu_seqlens[s]), int(w.cu_seqlens[s + 1])
+        for l in range(w.num_layers):
+            for hq in range(w.num_q_heads):
+                h = hq // w.group
+                sel = o["idx"][(s, l, h)]
+                kr, vr = O.compact(w.k[l, h, a:b], w.v[l, h, a:b], sel)
+                ref = O.decode_attention(O.decode_bf16(w.q_dec[l, s, hq]), O.decode_bf16(kr),
+                                         O.decode_bf16(vr), scale)
+                err = np.abs(out[l, s, hq] - ref).max()
+                assert err <= 2e-3 * np.abs(ref).max() + 1e-6, (s, l, hq, err)
