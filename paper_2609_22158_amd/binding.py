@@ -106,11 +106,15 @@ class StepKVError(RuntimeError):
         self.code = code
 
 
-def load(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load libstepkv.so and declare its signatures; raises if it is missing."""
+def load(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load libstepkv.so and declare its signatures; raises if it is missing.
+
+    The path defaults to the in-tree build; STEPKV_LIB names another build.
+    """
     global _lib
     if _lib is not None:
         return _lib
+    path = path or os.environ.get("STEPKV_LIB") or LIB_PATH
     if not os.path.exists(path):
         raise ImportError(
             f"{path} not found: build it with `python -m paper_2609_22158_amd.build` "

@@ -43,24 +43,31 @@ def _run(cmd):
     return msg
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link libstepkv.so; returns the library path."""
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose: bool = False, extra_flags=(), lib_path: str = LIB) -> str:
+    """Compile every source and link libstepkv.so; returns the library path.
+
+    extra_flags (e.g. -D tuning macros) and lib_path allow building variants
+    side by side with the default library.
+    """
+    tag = "" if lib_path == LIB else "_" + os.path.basename(lib_path).replace(".", "_")
+    bdir = BUILD + tag
+    os.makedirs(bdir, exist_ok=True)
     objs = []
     cmds = []
     for src in SOURCES:
-        obj = os.path.join(BUILD, src.rsplit(".", 1)[0] + ".o")
+        obj = os.path.join(bdir, src.rsplit(".", 1)[0] + ".o")
         lang = ["-x", "hip"] if src.endswith(".hip") else []
-        cmds.append([_hipcc(), *lang, *_flags(), "-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([_hipcc(), *lang, *_flags(), *extra_flags, "-c", os.path.join(CSRC, src),
+                     "-o", obj])
         objs.append(obj)
     with ThreadPoolExecutor(min(8, len(cmds))) as ex:
         for msg in ex.map(_run, cmds):
             if verbose and msg:
                 print(msg)
-    tmp = LIB + ".tmp"
+    tmp = lib_path + ".tmp"
     _run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib_path)
+    return lib_path
 
 
 if __name__ == "__main__":

@@ -24,18 +24,41 @@ namespace {
 
 constexpr int kThreads = 256;  // 4 waves: (row group) x (key group)
 
-// Byte offset of 16-byte piece p of key row r inside a K tile. Pieces are
-// XOR-swizzled by (r & 7) so that the 8 lanes of a ds_read_b128 phase, which
-// read the same logical piece of 8 consecutive rows, hit distinct banks.
+// XOR swizzle of the 16-byte pieces of key row r inside a K tile. The 16 lanes
+// of a ds_read_b128 phase read the same logical piece of 16 consecutive rows;
+// the swizzle spreads them over 16 distinct 16-byte bank groups (a 256-byte
+// row for d = 128; two 128-byte rows per bank line for d = 64).
+template <int D>
+__device__ __forceinline__ int swizzle(int r) {
+  return D == 128 ? (r & 15) : ((r >> 1) & 7);
+}
+
+// Byte offset of logical 16-byte piece p of key row r inside a K tile.
 template <int D>
 __device__ __forceinline__ int tile_offset(int r, int p) {
-  return r * (2 * D) + 16 * (p ^ (r & 7));
+  return r * (2 * D) + 16 * (p ^ swizzle<D>(r));
 }
 
 template <int N>
 __device__ __forceinline__ void wait_vmem() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
+
+// Wait until at most `ahead` tiles of NLD loads each are still in flight
+// (ahead = tiles issued after the one needed next, 0 <= ahead <= MAXA).
+template <int NLD, int MAXA>
+__device__ __forceinline__ void wait_tiles(int ahead) {
+  if constexpr (MAXA <= 0) {
+    wait_vmem<0>();
+  } else {
+    if (ahead >= MAXA) wait_vmem<MAXA * NLD>();
+    else wait_tiles<NLD, MAXA - 1>(ahead);
+  }
+}
+
+#ifndef STEPKV_SAL_RING_BYTES
+#define STEPKV_SAL_RING_BYTES 32768
+#endif
 
 // Make the compiler wait for the load that produced x here, once, instead of
 // at the first use inside the tile loop, where its wait would also drain the
@@ -94,7 +117,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   constexpr int TILE = 32 * KG;               // keys per workgroup iteration
   constexpr int KSTEPS = D / 16;              // MFMA k-steps
   constexpr int TILE_BYTES = TILE * 2 * D;
-  constexpr int NBUF = TILE_BYTES <= 16384 ? 4 : 2;
+  constexpr int NBUF = STEPKV_SAL_RING_BYTES / TILE_BYTES >= 2 ? STEPKV_SAL_RING_BYTES / TILE_BYTES : 2;
   constexpr int NLD = TILE_BYTES / (kThreads * 16);  // 16-byte loads per thread per tile
   static_assert(NLD >= 1, "tile too small");
   __shared__ __attribute__((aligned(16))) uint8_t kbuf[NBUF * TILE_BYTES];
@@ -148,7 +171,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
       const int o = 16 * (tid + kThreads * j);  // this lane's 16 bytes of the tile
       const int r = o / (2 * D);
       const int pp = (o % (2 * D)) / 16;
-      const int p = pp ^ (r & 7);
+      const int p = pp ^ swizzle<D>(r);
       const int key = min(key0 + t * TILE + r, ns - 1);  // tail rows re-read a valid key
       const uint16_t* src = kseq + (size_t)key * D + 8 * p;
       uint8_t* dst = base + 16 * (kThreads * j + 64 * wave);  // lane l lands at dst + 16 l
@@ -196,27 +219,17 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     }
   };
 
-#pragma unroll
-  for (int t = 0; t < NBUF - 1; ++t)
-    if (t < ntiles) issue_tile(t);
-
-  for (int t = 0; t < ntiles; ++t) {
-    const int ahead = min(NBUF - 2, ntiles - 1 - t);  // tiles issued after tile t
-    if (NBUF > 2 && ahead >= 2) wait_vmem<(NBUF > 2 ? 2 * NLD : 0)>();
-    else if (NBUF > 2 && ahead == 1) wait_vmem<(NBUF > 2 ? NLD : 0)>();
-    else wait_vmem<0>();
-    lds_barrier();
-    if (t + NBUF - 1 < ntiles) issue_tile(t + NBUF - 1);
-    if (PASS == 2 && t > 0) reduce_tile(t - 1);
-
+  const int kr = kg * 32 + col;
+  auto read_frags = [&](int t, bf16x8_t(&kf)[KSTEPS]) {
     const uint32_t tb = kbuf_lds + (t % NBUF) * TILE_BYTES;
-    const int kr = kg * 32 + col;
-    bf16x8_t kf[KSTEPS];
 #pragma unroll
     for (int st = 0; st < KSTEPS; ++st)
       kf[st] = lds_read_b128(tb + tile_offset<D>(kr, (D / 16) * hf + st));
     lds_settle(kf);
-    f32x16_t acc[2] = {f32x16_t{}, f32x16_t{}};
+  };
+  auto mfma_tile = [&](const bf16x8_t(&kf)[KSTEPS], f32x16_t(&acc)[2]) {
+    acc[0] = f32x16_t{};
+    acc[1] = f32x16_t{};
 #pragma unroll
     for (int st = 0; st < KSTEPS; ++st) {
 #pragma unroll
@@ -227,11 +240,12 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
           acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[b][st], kf[st], acc[b], 0, 0, 0);
       }
     }
-
+  };
+  // Softmax work on a finished tile t. Only the last tile can be partial.
+  auto finish_tile = [&](const f32x16_t(&acc)[2], int t, bool full) {
     if (PASS == 1) {
-      // lane: window row `col` of block b; keys kbase + 8*(j/4) + (j%4)
+      // lane: window row `col` of block b; keys t*TILE + kg*32 + 8*(j/4) + 4*hf + (j%4)
       const int kbase = t * TILE + kg * 32 + 4 * hf;
-      const bool full = (t + 1) * TILE <= nkeys;
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
         float v[16];
@@ -244,31 +258,117 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
 #pragma unroll
         for (int j = 1; j < 16; ++j) tmax = fmaxf(tmax, v[j]);
         const float mnew = fmaxf(m2[b], tmax * a.c);
-        if (mnew > m2[b]) {
-          zs[b] *= fast_exp2(m2[b] - mnew);
-          m2[b] = mnew;
-        }
-        if (m2[b] != -INFINITY) {
-          float sum = 0.f;
+        const float f = fast_exp2(m2[b] - mnew);  // rescale of the running sum
+        float p4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int j = 0; j < 16; ++j) sum += fast_exp2(fmaf(v[j], a.c, -m2[b]));
-          zs[b] += sum;
-        }
+        for (int j = 0; j < 16; ++j) p4[j & 3] += fast_exp2(fmaf(v[j], a.c, -mnew));
+        const float sum = (p4[0] + p4[1]) + (p4[2] + p4[3]);
+        // mnew = -inf only while every key seen by this lane was masked out
+        zs[b] = mnew == -INFINITY ? 0.f : fmaf(zs[b], f, sum);
+        m2[b] = mnew;
       }
     } else {
       // lane: key `col` of sub-tile kg; window rows 8*(j/4) + 4*hf + (j%4) of block b
-      float cs = 0.f;
+      float p4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) cs += fast_exp2(fmaf(acc[b][j], a.c, -lr[b][j]));
-      red[(t & 1) * kThreads + tid] = cs;
+        for (int j = 0; j < 16; ++j) p4[j & 3] += fast_exp2(fmaf(acc[b][j], a.c, -lr[b][j]));
+      red[(t & 1) * kThreads + tid] = (p4[0] + p4[1]) + (p4[2] + p4[3]);
     }
+  };
+  // One pipelined iteration on full tiles: the 2*KSTEPS MFMAs of tile t+1 are
+  // interleaved one by one with slices of the softmax work of tile t (two
+  // elements per slice), fenced so that the compiler keeps the order and the
+  // matrix core and the VALU of this wave run side by side.
+  auto body = [&](int t, f32x16_t(&cur)[2], f32x16_t(&nxt)[2], bf16x8_t(&kf)[KSTEPS]) {
+    static_assert(2 * KSTEPS * 2 == 32 || 2 * KSTEPS * 4 == 32, "slices cover 32 elements");
+    constexpr int PER = 32 / (2 * KSTEPS);  // elements of `cur` per MFMA
+    wait_tiles<NLD, NBUF - 2>(min(NBUF - 2, ntiles - 2 - t));  // tile t+1 has landed
+    lds_barrier();
+    if (t + NBUF < ntiles) issue_tile(t + NBUF);
+    if (PASS == 2 && t > 0) reduce_tile(t - 1);
+    const uint32_t tb = kbuf_lds + ((t + 1) % NBUF) * TILE_BYTES;
+#pragma unroll
+    for (int st = 0; st < KSTEPS; ++st)
+      kf[st] = lds_read_b128(tb + tile_offset<D>(kr, (D / 16) * hf + st));
+    // pass 1: the tile's row maxima and the rescale factors, while LDS reads fly
+    float mnew[2], fsc[2];
+    if (PASS == 1) {
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        float tmax = cur[b][0];
+#pragma unroll
+        for (int j = 1; j < 16; ++j) tmax = fmaxf(tmax, cur[b][j]);
+        mnew[b] = fmaxf(m2[b], tmax * a.c);
+        fsc[b] = fast_exp2(m2[b] - mnew[b]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    lds_settle(kf);
+    nxt[0] = f32x16_t{};
+    nxt[1] = f32x16_t{};
+    float p4[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+    for (int i = 0; i < 2 * KSTEPS; ++i) {
+      const int st = i >> 1, b = i & 1;
+      if (PASS == 1)
+        nxt[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qf[b][st], nxt[b], 0, 0, 0);
+      else
+        nxt[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[b][st], kf[st], nxt[b], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int e = i * PER; e < (i + 1) * PER; ++e) {
+        const int bb = e >> 4, j = e & 15;
+        const float ref = PASS == 1 ? mnew[bb] : lr[bb][j];
+        p4[bb][j & 3] += fast_exp2(fmaf(cur[bb][j], a.c, -ref));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (PASS == 1) {
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        // full tile: mnew is finite; fsc = 0 on the first tile (m2 = -inf)
+        const float sum = (p4[b][0] + p4[b][1]) + (p4[b][2] + p4[b][3]);
+        zs[b] = fmaf(zs[b], fsc[b], sum);
+        m2[b] = mnew[b];
+        settle(zs[b]);  // keeps this iteration's VALU work inside this iteration
+      }
+    } else {
+      red[(t & 1) * kThreads + tid] =
+          ((p4[0][0] + p4[0][1]) + (p4[0][2] + p4[0][3])) +
+          ((p4[1][0] + p4[1][1]) + (p4[1][2] + p4[1][3]));
+    }
+  };
+
+#pragma unroll
+  for (int t = 0; t < NBUF - 1; ++t)
+    if (t < ntiles) issue_tile(t);
+  wait_tiles<NLD, NBUF - 2>(min(NBUF - 2, ntiles - 1));  // tile 0 has landed
+  lds_barrier();
+  if (NBUF - 1 < ntiles) issue_tile(NBUF - 1);
+  bf16x8_t kf[KSTEPS];
+  f32x16_t acc_a[2], acc_b[2];
+  read_frags(0, kf);
+  mfma_tile(kf, acc_a);
+  int t = 0;
+  for (; t + 2 < ntiles; t += 2) {  // ping-pong accumulators, no register copies
+    body(t, acc_a, acc_b, kf);
+    body(t + 1, acc_b, acc_a, kf);
   }
+  f32x16_t(&last)[2] = (t + 1 < ntiles) ? acc_b : acc_a;
+  if (t + 1 < ntiles) {
+    body(t, acc_a, acc_b, kf);
+    ++t;
+  }
+  // t = ntiles - 1: the last, possibly partial, tile
+  lds_barrier();
+  if (PASS == 2 && t > 0) reduce_tile(t - 1);
+  finish_tile(last, t, (t + 1) * TILE <= nkeys);
 
   if (PASS == 2) {
     lds_barrier();
-    if (ntiles > 0) reduce_tile(ntiles - 1);
+    reduce_tile(t);
     return;
   }
 
