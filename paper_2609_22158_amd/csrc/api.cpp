@@ -250,6 +250,7 @@ int run_priority(const stepkv_problem* pb, const stepkv_params* prm, const float
   fa.total_steps = pb->cu_steps_host[pb->num_seqs];
   fa.half = prm->pool_kernel / 2;
   fa.max_steps = std::max(max_steps_per_seq(pb), 1);
+  fa.max_len = max_seqlen(pb);
   fa.alpha = prm->alpha;
   fa.beta = prm->beta;
   return hip_status(launch_fuse(fa, st));

@@ -4,8 +4,15 @@
 //   Th_i = U_i / max_{prunable} U                   (the 1/k cancels)
 //   P_i  = alpha * Th_i + beta * S[step_ids[i]]     (prunable; -inf if protected)
 // Step statistics (count, max and fixed-point sum of Th over each step's
-// prunable tokens) use one wave ballot per distinct step id in the wave and
-// LDS atomics, so the result does not depend on the order of the atomics.
+// prunable tokens) are segmented reductions keyed by step id: partial results
+// over runs of one step go to LDS atomics in unsigned fixed point, so the
+// result does not depend on the order of the atomics.
+//
+// Fast path (N_s <= 32768, pooling window <= 9): the sequence is staged in
+// LDS in batches of 8192 positions with coalesced loads; each thread pools a
+// run of 8 consecutive positions from registers and keeps its 32 pooled
+// values in registers for the second sweep. Otherwise the sequence streams
+// through a 1024-position LDS tile.
 #include "common.h"
 #include "internal.h"
 
@@ -23,10 +30,220 @@ struct StatOut {  // layout of stepkv_step_stat
   uint64_t sum_q32;
 };
 
-__global__ __launch_bounds__(kThreads) void fuse_kernel(FuseArgs a) {
+constexpr int kWaves = kThreads / kWave;
+constexpr int kBatch = 8192;             // positions staged in LDS per batch
+constexpr int kRun = kBatch / kThreads;  // consecutive positions per thread per batch
+constexpr int kMaxBatches = 4;           // fast path: N_s <= 32768
+constexpr int kFastHalf = 4;             // fast path: pooling window <= 9
+
+// Per-step statistics tables in dynamic LDS (after the utility table).
+struct StepTables {
+  float* util;
+  uint32_t* cnt;
+  uint32_t* mx;
+  unsigned long long* sum;
+};
+
+__device__ __forceinline__ StepTables step_tables(uint8_t* dyn, int max_steps) {
+  StepTables t;
+  t.util = reinterpret_cast<float*>(dyn);
+  t.cnt = reinterpret_cast<uint32_t*>(dyn) + max_steps;
+  t.mx = t.cnt + max_steps;
+  t.sum = reinterpret_cast<unsigned long long*>(dyn + ((size_t)(3 * max_steps) * 4 + 7) / 8 * 8);
+  return t;
+}
+
+__device__ __forceinline__ void flush_stat(const StepTables& t, int k, uint32_t cnt, float mx,
+                                           float sum) {
+  atomicAdd(&t.cnt[k], cnt);
+  atomicMax(&t.mx[k], __float_as_uint(mx));  // Th >= 0: bit order = value order
+  atomicAdd(&t.sum[k], (unsigned long long)((double)sum * 4294967296.0 + 0.5));
+}
+
+__device__ __forceinline__ void write_stats(const FuseArgs& a, const StepTables& t, int lh,
+                                            int st0, int nsteps) {
+  StatOut* so = reinterpret_cast<StatOut*>(a.stats) + (size_t)lh * a.total_steps + st0;
+  for (int k = threadIdx.x; k < nsteps; k += kThreads) {
+    StatOut r;
+    r.count = t.cnt[k];
+    r.max_saliency = __uint_as_float(t.mx[k]);
+    r.sum_q32 = t.sum[k];
+    so[k] = r;
+  }
+}
+
+template <int HALF>
+__global__ __launch_bounds__(kThreads) void fuse_batched_kernel(FuseArgs a) {
+  // stage[kFastHalf + p] holds batch position p; runs of 8 positions are read
+  // as aligned 16-byte vectors, global traffic stays coalesced (tid + 1024 j)
+  __shared__ __attribute__((aligned(16))) float stage[kFastHalf + kBatch + kFastHalf];
+  __shared__ __attribute__((aligned(16))) uint8_t pstage[kBatch];  // prunable flags
+  __shared__ float wred[kWaves];
+  extern __shared__ uint8_t dyn[];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int s = blockIdx.x / a.LH, lh = blockIdx.x - s * a.LH;
+  const int seq0 = a.cu_seqlens[s];
+  const int ns = a.cu_seqlens[s + 1] - seq0;
+  const int st0 = a.cu_steps[s];
+  const int nsteps = a.cu_steps[s + 1] - st0;
+  const float* __restrict__ A = a.sal + (size_t)lh * a.ntot + seq0;
+  const uint8_t* __restrict__ prot = a.prot + seq0;
+  const int32_t* __restrict__ sid = a.step_ids + seq0;
+  const bool stats = a.stats != nullptr;
+  const StepTables tabs = step_tables(dyn, a.max_steps);
+  for (int k = tid; k < nsteps; k += kThreads) {
+    tabs.util[k] = a.util[st0 + k];
+    if (stats) {
+      tabs.cnt[k] = 0u;
+      tabs.mx[k] = 0u;
+      tabs.sum[k] = 0ull;
+    }
+  }
+  const int nb = (ns + kBatch - 1) / kBatch;
+  constexpr int J = kRun * kMaxBatches;  // 32 coalesced slots: position tid + 1024 j
+
+  // every A and protected-flag load of the sequence, issued up front
+  float x[J];
+  uint32_t pb[J];
+  if (ns > 0) {
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int ic = min(tid + kThreads * j, ns - 1);
+      x[j] = A[ic];
+      pb[j] = prot[ic];
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const bool pr = ns > 0 && tid + kThreads * j < ns && pb[j] == 0;
+    x[j] = pr ? x[j] : 0.f;
+    pb[j] = pr ? 1u : 0u;
+  }
+
+  float u[kMaxBatches][kRun];
+  uint32_t prun = 0u;  // bit kRun*b + r: position b*kBatch + kRun*tid + r is prunable
+  float mloc = 0.f;    // U >= 0, and Th = 0 everywhere when the max is 0
+#pragma unroll
+  for (int b = 0; b < kMaxBatches; ++b) {
+    if (b < nb) {
+#pragma unroll
+      for (int jj = 0; jj < kRun; ++jj) {
+        stage[kFastHalf + tid + kThreads * jj] = x[kRun * b + jj];
+        pstage[tid + kThreads * jj] = (uint8_t)pb[kRun * b + jj];
+      }
+      // halos: the 4 positions before the batch sit in the previous batch's last
+      // slot of threads 1020..1023, the 4 after it in the next batch's first slot
+      if (tid >= kThreads - kFastHalf)
+        stage[tid - (kThreads - kFastHalf)] = b > 0 ? x[b > 0 ? kRun * b - 1 : 0] : 0.f;
+      if (tid < kFastHalf)
+        stage[kFastHalf + kBatch + tid] = b + 1 < kMaxBatches ? x[b + 1 < kMaxBatches ? kRun * (b + 1) : 0] : 0.f;
+      __syncthreads();
+      // run: positions kRun*tid - 4 .. kRun*tid + 11 of the batch
+      float v[16];
+      const float4* sp = reinterpret_cast<const float4*>(stage + kRun * tid);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 f = sp[q];
+        v[4 * q] = f.x;
+        v[4 * q + 1] = f.y;
+        v[4 * q + 2] = f.z;
+        v[4 * q + 3] = f.w;
+      }
+      const uint64_t fl = *reinterpret_cast<const uint64_t*>(&pstage[kRun * tid]);
+#pragma unroll
+      for (int r = 0; r < kRun; ++r) {
+        float acc = 0.f;
+#pragma unroll
+        for (int o = 0; o <= 2 * HALF; ++o) acc += v[kFastHalf - HALF + r + o];
+        u[b][r] = acc;
+        const bool pr = (fl >> (8 * r)) & 0xFFull;
+        prun |= (pr ? 1u : 0u) << (kRun * b + r);
+        mloc = pr ? fmaxf(mloc, acc) : mloc;
+      }
+      __syncthreads();  // the next batch reuses the stage
+    }
+  }
+  mloc = wave_max(mloc);
+  if (lane == 0) wred[wave] = mloc;
+  // step ids of the sequence, coalesced, issued while the maximum is reduced
+  int32_t sv[J];
+  if (ns > 0) {
+#pragma unroll
+    for (int j = 0; j < J; ++j) sv[j] = sid[min(tid + kThreads * j, ns - 1)];
+  }
+  __syncthreads();
+  float M = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wred[w]);
+  const float inv = M > 0.f ? 1.0f / M : 0.f;
+
+  // ---- sweep 2: normalise, fuse; the run's scores go back through the stage
+  float* __restrict__ out = a.scores + (size_t)lh * a.ntot + seq0;
+  int32_t* istage = reinterpret_cast<int32_t*>(stage);
+#pragma unroll
+  for (int b = 0; b < kMaxBatches; ++b) {
+    if (b < nb) {
+#pragma unroll
+      for (int jj = 0; jj < kRun; ++jj) istage[tid + kThreads * jj] = sv[kRun * b + jj];
+      __syncthreads();
+      const int4 k0 = reinterpret_cast<const int4*>(istage + kRun * tid)[0];
+      const int4 k1 = reinterpret_cast<const int4*>(istage + kRun * tid)[1];
+      const int kr[kRun] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
+      float pv[kRun];
+      int cur = -1;
+      uint32_t ccount = 0u;
+      float cmax = 0.f, csum = 0.f;
+#pragma unroll
+      for (int r = 0; r < kRun; ++r) {
+        const bool pr = (prun >> (kRun * b + r)) & 1u;
+        const int kk = kr[r];
+        const bool ok = pr && kk >= 0 && kk < nsteps;
+        const float th = u[b][r] * inv;
+        const float util = ok ? tabs.util[ok ? kk : 0] : 0.f;
+        pv[r] = pr ? fmaf(a.alpha, th, a.beta * util) : -INFINITY;
+        if (stats) {
+          const int key = ok ? kk : -1;
+          if (key != cur) {
+            if (cur >= 0) flush_stat(tabs, cur, ccount, cmax, csum);
+            cur = key;
+            ccount = 0u;
+            cmax = 0.f;
+            csum = 0.f;
+          }
+          if (key >= 0) {
+            ++ccount;
+            cmax = fmaxf(cmax, th);
+            csum += th;
+          }
+        }
+      }
+      if (stats && cur >= 0) flush_stat(tabs, cur, ccount, cmax, csum);
+      __syncthreads();  // step ids read before the stage takes the scores
+      float4* wp = reinterpret_cast<float4*>(stage + kRun * tid);
+      wp[0] = make_float4(pv[0], pv[1], pv[2], pv[3]);
+      wp[1] = make_float4(pv[4], pv[5], pv[6], pv[7]);
+      __syncthreads();
+#pragma unroll
+      for (int jj = 0; jj < kRun; ++jj) {
+        const int i = b * kBatch + tid + kThreads * jj;
+        if (i < ns) out[i] = stage[tid + kThreads * jj];
+      }
+      __syncthreads();  // the next batch reuses the stage
+    }
+  }
+  if (stats) {
+    __syncthreads();
+    write_stats(a, tabs, lh, st0, nsteps);
+  }
+}
+
+// General path: the sequence streams through a 1024-position tile.
+__global__ __launch_bounds__(kThreads) void fuse_stream_kernel(FuseArgs a) {
   __shared__ float tile[kThreads + 2 * kMaxHalf];
-  __shared__ float wred[kThreads / kWave];
-  extern __shared__ uint8_t dyn[];  // per-step tables: count, max bits, q32 sum
+  __shared__ float wred[kWaves];
+  extern __shared__ uint8_t dyn[];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -40,99 +257,72 @@ __global__ __launch_bounds__(kThreads) void fuse_kernel(FuseArgs a) {
   const int32_t* __restrict__ sid = a.step_ids + seq0;
   const int half = a.half;
   const bool stats = a.stats != nullptr;
-
-  // dynamic LDS: count[max_steps], max bits[max_steps], then 8-aligned q32 sums
-  uint32_t* s_cnt = reinterpret_cast<uint32_t*>(dyn);
-  uint32_t* s_max = s_cnt + a.max_steps;
-  unsigned long long* s_sum =
-      reinterpret_cast<unsigned long long*>(dyn + ((size_t)(2 * a.max_steps) * 4 + 7) / 8 * 8);
-  if (stats) {
-    for (int k = tid; k < nsteps; k += kThreads) {
-      s_cnt[k] = 0u;
-      s_max[k] = 0u;
-      s_sum[k] = 0ull;
+  const StepTables tabs = step_tables(dyn, a.max_steps);
+  for (int k = tid; k < nsteps; k += kThreads) {
+    tabs.util[k] = a.util[st0 + k];
+    if (stats) {
+      tabs.cnt[k] = 0u;
+      tabs.mx[k] = 0u;
+      tabs.sum[k] = 0ull;
     }
   }
-
-  // masked saliency A_j [j prunable], zero outside the sequence
   auto masked = [&](int j) -> float {
     return (j >= 0 && j < ns && prot[j] == 0) ? A[j] : 0.f;
   };
-  // U for position base + tid, reading the tile staged for [base - half, base + 1024 + half)
-  auto pooled_tile = [&](int base) -> float {
+  auto pooled = [&](int base) -> float {
     tile[tid + half] = masked(base + tid);
     if (tid < half) tile[tid] = masked(base - half + tid);
     if (tid < half) tile[kThreads + half + tid] = masked(base + kThreads + tid);
     __syncthreads();
-    float u = 0.f;
-    for (int o = 0; o <= 2 * half; ++o) u += tile[tid + o];
+    float acc = 0.f;
+    for (int o = 0; o <= 2 * half; ++o) acc += tile[tid + o];
     __syncthreads();
-    return u;
+    return acc;
   };
-
-  // ---- sweep 1: max of U over prunable tokens
-  float mloc = 0.f;  // U >= 0, and Th = 0 everywhere when the max is 0
+  float mloc = 0.f;
   for (int base = 0; base < ns; base += kThreads) {
-    const float u = pooled_tile(base);
+    const float uu = pooled(base);
     const int i = base + tid;
-    if (i < ns && prot[i] == 0) mloc = fmaxf(mloc, u);
+    if (i < ns && prot[i] == 0) mloc = fmaxf(mloc, uu);
   }
   mloc = wave_max(mloc);
   if (lane == 0) wred[wave] = mloc;
   __syncthreads();
   float M = 0.f;
-#pragma unroll
-  for (int w = 0; w < kThreads / kWave; ++w) M = fmaxf(M, wred[w]);
-
-  // ---- sweep 2: normalise, fuse, write, segmented statistics
+  for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wred[w]);
+  const float inv = M > 0.f ? 1.0f / M : 0.f;
   float* __restrict__ out = a.scores + (size_t)lh * a.ntot + seq0;
   for (int base = 0; base < ns; base += kThreads) {
-    const float u = pooled_tile(base);
+    const float uu = pooled(base);
     const int i = base + tid;
-    int k = -1;
+    int kk = -1;
     float th = 0.f;
     if (i < ns) {
-      if (prot[i] == 0) {
-        th = M > 0.f ? u / M : 0.f;
-        k = sid[i];
-        const bool ok = k >= 0 && k < nsteps;
-        const float util = ok ? a.util[st0 + k] : 0.f;
-        out[i] = a.alpha * th + a.beta * util;
-        if (!ok) k = -1;
-      } else {
-        out[i] = -INFINITY;
-      }
+      const bool pr = prot[i] == 0;
+      kk = sid[i];
+      const bool ok = pr && kk >= 0 && kk < nsteps;
+      th = uu * inv;
+      out[i] = pr ? fmaf(a.alpha, th, a.beta * (ok ? tabs.util[kk] : 0.f)) : -INFINITY;
+      if (!ok) kk = -1;
     }
     if (stats) {
-      // one round per distinct step id present in this wave
-      uint64_t pending = ballot(k >= 0);
+      // one wave ballot per distinct step id present in the wave
+      uint64_t pending = ballot(kk >= 0);
       while (pending) {
         const int leader = __builtin_ctzll(pending);
-        const int key = __shfl(k, leader, kWave);
-        const uint64_t grp = ballot(k == key);
-        const float mine = (k == key) ? th : 0.f;
+        const int key = __builtin_amdgcn_readlane(kk, leader);
+        const uint64_t grp = ballot(kk == key);
+        const float mine = (kk == key) ? th : 0.f;
         const float sum = wave_sum(mine);
         const float mx = wave_max(mine);
-        if (lane == leader) {
-          atomicAdd(&s_cnt[key], (uint32_t)__popcll(grp));
-          atomicMax(&s_max[key], __float_as_uint(mx));  // th >= 0: bit order = value order
-          atomicAdd(&s_sum[key], (unsigned long long)((double)sum * 4294967296.0 + 0.5));
-        }
+        if (lane == leader) flush_stat(tabs, key, (uint32_t)__popcll(grp), mx, sum);
         pending &= ~grp;
       }
     }
   }
-
   if (stats) {
     __syncthreads();
-    StatOut* so = reinterpret_cast<StatOut*>(a.stats) + (size_t)lh * a.total_steps + st0;
-    for (int k = tid; k < nsteps; k += kThreads) {
-      StatOut r;
-      r.count = s_cnt[k];
-      r.max_saliency = __uint_as_float(s_max[k]);
-      r.sum_q32 = s_sum[k];
-      so[k] = r;
-    }
+    write_stats(a, tabs, lh, st0, nsteps);
   }
 }
 
@@ -140,9 +330,20 @@ __global__ __launch_bounds__(kThreads) void fuse_kernel(FuseArgs a) {
 
 hipError_t launch_fuse(const FuseArgs& a, hipStream_t st) {
   if (a.S * a.LH == 0) return hipSuccess;
-  size_t dyn = 0;
-  if (a.stats) dyn = ((size_t)(2 * a.max_steps) * 4 + 7) / 8 * 8 + (size_t)a.max_steps * 8;
-  hipLaunchKernelGGL(fuse_kernel, dim3(a.S * a.LH), dim3(kThreads), dyn, st, a);
+  size_t dyn = (size_t)a.max_steps * 4;
+  if (a.stats) dyn = ((size_t)(3 * a.max_steps) * 4 + 7) / 8 * 8 + (size_t)a.max_steps * 8;
+  const dim3 grid(a.S * a.LH), block(kThreads);
+  if (a.max_len <= kBatch * kMaxBatches && a.half <= kFastHalf) {
+    switch (a.half) {
+      case 0: hipLaunchKernelGGL(fuse_batched_kernel<0>, grid, block, dyn, st, a); break;
+      case 1: hipLaunchKernelGGL(fuse_batched_kernel<1>, grid, block, dyn, st, a); break;
+      case 2: hipLaunchKernelGGL(fuse_batched_kernel<2>, grid, block, dyn, st, a); break;
+      case 3: hipLaunchKernelGGL(fuse_batched_kernel<3>, grid, block, dyn, st, a); break;
+      default: hipLaunchKernelGGL(fuse_batched_kernel<4>, grid, block, dyn, st, a); break;
+    }
+  } else {
+    hipLaunchKernelGGL(fuse_stream_kernel, grid, block, dyn, st, a);
+  }
   return hipGetLastError();
 }
 

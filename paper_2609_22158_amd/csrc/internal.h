@@ -39,7 +39,7 @@ struct FuseArgs {
   const float* util;         // [cu_steps[S]]
   float* scores;             // [L*Hkv][Ntot]
   void* stats;               // stepkv_step_stat [L*Hkv][cu_steps[S]] or null
-  int S, LH, ntot, total_steps, half, max_steps;
+  int S, LH, ntot, total_steps, half, max_steps, max_len;
   float alpha, beta;
 };
 hipError_t launch_fuse(const FuseArgs& a, hipStream_t st);
