@@ -41,7 +41,93 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget for the oracle CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="run one plain device copy of this size (HBM counter calibration)")
+    ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
+                         "WRITE_SIZE) of a --copy-probe-mib run into profiles/traffic.json")
     return ap.parse_args()
+
+
+SALIENCY_KERNELS = ("saliency_kernel", "lse_combine_kernel", "chunk_plan_kernel")
+
+
+def record_traffic(args) -> None:
+    """HBM bytes per saliency launch, scaled by the counters' reading of a plain copy."""
+    import csv
+    from collections import defaultdict
+
+    def per_dispatch(path, counter):
+        vals = defaultdict(float)
+        names = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            vals[r["Dispatch_Id"]] += float(r["Counter_Value"])  # KiB, summed over instances
+            names[r["Dispatch_Id"]] = r["Kernel_Name"]
+        return vals, names
+
+    probe = args.copy_probe_mib << 20
+    if probe <= 0:
+        sys.exit("--record-traffic needs the --copy-probe-mib size the counters were taken with")
+    out = {}
+    for counter, path in (("FETCH_SIZE", args.record_traffic[0]),
+                          ("WRITE_SIZE", args.record_traffic[1])):
+        vals, names = per_dispatch(path, counter)
+        copies = [d for d in vals if "copyBuffer" in names[d]]
+        cal = probe / (max(vals[d] for d in copies) * 1024.0)  # bytes per counted byte
+        per_kernel = defaultdict(list)
+        for d, v in vals.items():
+            for k in SALIENCY_KERNELS:
+                if k in names[d]:
+                    per_kernel[k].append(v * 1024.0 * cal)
+        launches = len(per_kernel["chunk_plan_kernel"])  # one per saliency launch
+        out[counter] = {"calibration": cal, "launches": launches,
+                        "bytes": sum(sum(v) for v in per_kernel.values()) / launches,
+                        "per_kernel": {k: sum(v) / launches for k, v in per_kernel.items()}}
+    budget = args.budget or 1024
+    key = f"{args.workload}_b{budget}_w{args.window or 64}"
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        db = json.load(open(path))
+    except (OSError, ValueError):
+        db = {}
+    db[key] = {
+        "saliency_source_sha256": source_digest(),
+        "hbm_bytes_per_launch": round(out["FETCH_SIZE"]["bytes"] + out["WRITE_SIZE"]["bytes"]),
+        "fetch_bytes_per_launch": round(out["FETCH_SIZE"]["bytes"]),
+        "write_bytes_per_launch": round(out["WRITE_SIZE"]["bytes"]),
+        "fetch_calibration": out["FETCH_SIZE"]["calibration"],
+        "write_calibration": out["WRITE_SIZE"]["calibration"],
+        "per_kernel_fetch_bytes": out["FETCH_SIZE"]["per_kernel"],
+        "per_kernel_write_bytes": out["WRITE_SIZE"]["per_kernel"],
+        "copy_probe_bytes": probe,
+    }
+    with open(path, "w") as f:
+        json.dump(db, f, indent=1, sort_keys=True)
+    print(json.dumps(db[key]))
+
+
+def source_digest() -> str:
+    """sha256 of the saliency kernel source: traffic figures are valid for it only."""
+    import hashlib
+
+    path = os.path.join(ROOT, "paper_2609_22158_amd", "csrc", "saliency.hip")
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def recorded_traffic(workload: str, budget: int, window: int):
+    """HBM bytes per saliency launch from the committed counter runs, or None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f).get(f"{workload}_b{budget}_w{window}")
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("saliency_source_sha256") != source_digest():
+        return None  # kernel changed since the counters were taken
+    return rec.get("hbm_bytes_per_launch")
 
 
 def cpu_baseline(w, budget, seconds):
@@ -80,6 +166,9 @@ def cpu_baseline(w, budget, seconds):
 
 def main():
     args = parse()
+    if args.record_traffic:
+        record_traffic(args)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}): "
@@ -149,6 +238,13 @@ def main():
         step()
     torch.cuda.synchronize()
     assert int(cu_ret[-1].item()) == out_rows
+    if args.copy_probe_mib > 0:  # one plain copy of known size, for counter calibration
+        n = args.copy_probe_mib << 20
+        src_buf = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst_buf = torch.empty_like(src_buf)
+        dst_buf.copy_(src_buf)
+        torch.cuda.synchronize()
+        del src_buf, dst_buf
 
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
@@ -182,7 +278,8 @@ def main():
     achieved_tflops = sal_flops / t_sal / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved_tflops, 2),
                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved_tflops / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                "frac": round(achieved_tflops / BF16_PEAK_TFLOPS, 4),
+                "traffic": recorded_traffic(args.workload, budget, w.window),
                 "kernel": "saliency (two MFMA sweeps over K)"}
     hbm = {"saliency_gbps": round(sal_bytes / t_sal / 1e9, 1),
            "saliency_frac": round(sal_bytes / t_sal / 1e9 / HBM_PEAK_GBS, 4),
