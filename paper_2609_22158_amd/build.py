@@ -65,7 +65,7 @@ def build(verbose: bool = False, extra_flags=(), lib_path: str = LIB) -> str:
             if verbose and msg:
                 print(msg)
     tmp = lib_path + ".tmp"
-    _run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
+    _run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Wl,-z,defs", "-o", tmp, *objs])
     os.replace(tmp, lib_path)
     return lib_path
 

@@ -19,6 +19,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace stepkv {
 namespace {
 
@@ -68,14 +70,23 @@ __device__ __forceinline__ void settle(T& x) {
   asm volatile("" : "+v"(x));
 }
 
-// One 16-byte LDS read of the K ring. Issued as assembly so that the compiler,
-// which cannot tell the ring slots apart, does not put a vmcnt(0) (a wait for
-// the whole prefetch ring) in front of it; completion is awaited explicitly
-// with lds_settle.
+// One 16-byte LDS read of the K ring at addr + OFF. Issued as assembly so
+// that the compiler, which cannot tell the ring slots apart, does not put a
+// vmcnt(0) (a wait for the whole prefetch ring) in front of it; completion is
+// awaited explicitly with lds_wait / lds_settle.
+template <int OFF>
 __device__ __forceinline__ bf16x8_t lds_read_b128(uint32_t addr) {
   bf16x8_t v;
-  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF) : "memory");
   return v;
+}
+
+// Wait until at most N LDS operations of this wave are outstanding. LDS
+// returns in issue order, so after issuing fragments 0..F-1 back to back,
+// lds_wait<F-1-k>(frag[k]) makes fragment k (and all before it) usable.
+template <int N>
+__device__ __forceinline__ void lds_wait(bf16x8_t& f) {
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(f) : "n"(N));
 }
 
 template <int N>
@@ -109,17 +120,34 @@ __global__ void chunk_plan_kernel(const int32_t* __restrict__ cu_seqlens,
   }
 }
 
+// Calls f(std::integral_constant<int, I>{}) for I = B .. E-1, unrolled.
+template <int B, int E, typename F>
+__host__ __device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 // D: head dim. RG: row groups of 64 window rows (1, 2 or 4); the 4 / RG
 // waves per row group split each key tile into 32-key sub-tiles.
+//
+// The tile loop is unrolled by the ring depth so that every ring slot is a
+// compile-time LDS offset: fragment reads use per-lane addresses computed
+// once plus an immediate, and full tiles load from a scalar base plus
+// per-lane constant offsets.
 template <int D, int RG, int PASS>
 __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   constexpr int KG = 4 / RG;
   constexpr int TILE = 32 * KG;               // keys per workgroup iteration
   constexpr int KSTEPS = D / 16;              // MFMA k-steps
   constexpr int TILE_BYTES = TILE * 2 * D;
-  constexpr int NBUF = STEPKV_SAL_RING_BYTES / TILE_BYTES >= 2 ? STEPKV_SAL_RING_BYTES / TILE_BYTES : 2;
+  // ring slots: an even count, 2 to 8
+  constexpr int NBUF_FIT = STEPKV_SAL_RING_BYTES / TILE_BYTES;
+  constexpr int NBUF = NBUF_FIT >= 8 ? 8 : (NBUF_FIT >= 2 ? NBUF_FIT & ~1 : 2);
   constexpr int NLD = TILE_BYTES / (kThreads * 16);  // 16-byte loads per thread per tile
   static_assert(NLD >= 1, "tile too small");
+  static_assert((NBUF - 1) * TILE_BYTES < 65536, "ring offset must fit the ds_read offset field");
   __shared__ __attribute__((aligned(16))) uint8_t kbuf[NBUF * TILE_BYTES];
   __shared__ float red[2 * kThreads];
 
@@ -132,10 +160,10 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   // ---- work item: (head lh, sequence s, chunk c)
   const int LH = a.L * a.Hkv;
   int lh = blockIdx.x / a.total_chunks;
-  const int rem = blockIdx.x - lh * a.total_chunks;
+  const int rem_blk = blockIdx.x - lh * a.total_chunks;
   if (PASS == 2) lh = LH - 1 - lh;  // pass 2 starts where pass 1 ended (cache reuse)
-  const int s = segment_of(a.cu_chunks, a.S, rem);
-  const int c = rem - a.cu_chunks[s];
+  const int s = segment_of(a.cu_chunks, a.S, rem_blk);
+  const int c = rem_blk - a.cu_chunks[s];
   const int l = lh / a.Hkv, h = lh - l * a.Hkv;
   const int seq0 = a.cu_seqlens[s];
   const int ns = a.cu_seqlens[s + 1] - seq0;
@@ -162,25 +190,60 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     }
   }
 
+  // ---- K ring: this lane's 16-byte pieces of a tile (HBM side) ...
+  const char* __restrict__ kbytes = reinterpret_cast<const char*>(kseq);
+  uint32_t ld_off[NLD];  // byte offset from the tile's first key row
+  int ld_row[NLD];       // key row inside the tile
+#pragma unroll
+  for (int j = 0; j < NLD; ++j) {
+    const int o = 16 * (tid + kThreads * j);
+    const int r = o / (2 * D);
+    const int p = ((o % (2 * D)) / 16) ^ swizzle<D>(r);
+    ld_row[j] = r;
+    ld_off[j] = r * (2 * D) + 16 * p;
+  }
+  // ... and the LDS side: fragment st of this lane's key row
   const uint32_t kbuf_lds = static_cast<uint32_t>(
       reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint8_t*)kbuf));
-  auto issue_tile = [&](int t) {
-    uint8_t* base = kbuf + (t % NBUF) * TILE_BYTES;
+  const int kr = kg * 32 + col;
+  uint32_t fa[KSTEPS];
 #pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const int o = 16 * (tid + kThreads * j);  // this lane's 16 bytes of the tile
-      const int r = o / (2 * D);
-      const int pp = (o % (2 * D)) / 16;
-      const int p = pp ^ swizzle<D>(r);
-      const int key = min(key0 + t * TILE + r, ns - 1);  // tail rows re-read a valid key
-      const uint16_t* src = kseq + (size_t)key * D + 8 * p;
-      uint8_t* dst = base + 16 * (kThreads * j + 64 * wave);  // lane l lands at dst + 16 l
-      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0,
-                                       0);
+  for (int st = 0; st < KSTEPS; ++st) fa[st] = kbuf_lds + tile_offset<D>(kr, (D / 16) * hf + st);
+
+  auto issue_tile = [&](int t, auto slot_c) {
+    constexpr int slot = decltype(slot_c)::value;
+    const int kt = key0 + t * TILE;  // first key of the tile
+    uint8_t* base = kbuf + slot * TILE_BYTES;
+    if (kt + TILE <= ns) {
+      const char* tb = kbytes + (size_t)kt * (2 * D);
+#pragma unroll
+      for (int j = 0; j < NLD; ++j)
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(tb + ld_off[j]),
+                                         (__attribute__((address_space(3))) void*)(
+                                             base + 16 * (kThreads * j + 64 * wave)),
+                                         16, 0, 0);
+    } else {  // tail rows re-read the last valid key
+#pragma unroll
+      for (int j = 0; j < NLD; ++j) {
+        const int key = min(kt + ld_row[j], ns - 1);
+        const char* src = kbytes + (size_t)key * (2 * D) + (ld_off[j] - ld_row[j] * (2 * D));
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(src),
+                                         (__attribute__((address_space(3))) void*)(
+                                             base + 16 * (kThreads * j + 64 * wave)),
+                                         16, 0, 0);
+      }
     }
   };
+  auto read_frags = [&](auto slot_c, bf16x8_t(&kf)[KSTEPS]) {
+    constexpr int slot = decltype(slot_c)::value;
+#pragma unroll
+    for (int st = 0; st < KSTEPS; ++st) kf[st] = lds_read_b128<slot * TILE_BYTES>(fa[st]);
+  };
 
-  // pass 1 state: per lane, per row block, running log2-domain max and sum
+  // pass 1 state: per lane and row block, a log2-domain reference m2 and the
+  // sum of exp2(c z - m2) over the keys seen so far (the pair stands for
+  // 2^m2 * zs). Full tiles keep m2 and only move it up to the tile's maximum,
+  // rescaling the sum, when the sum would exceed 2^64.
   float m2[2] = {-INFINITY, -INFINITY};
   float zs[2] = {0.f, 0.f};
   // pass 2 state: log2-domain LSE of the 16 rows this lane holds per block
@@ -219,14 +282,6 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     }
   };
 
-  const int kr = kg * 32 + col;
-  auto read_frags = [&](int t, bf16x8_t(&kf)[KSTEPS]) {
-    const uint32_t tb = kbuf_lds + (t % NBUF) * TILE_BYTES;
-#pragma unroll
-    for (int st = 0; st < KSTEPS; ++st)
-      kf[st] = lds_read_b128(tb + tile_offset<D>(kr, (D / 16) * hf + st));
-    lds_settle(kf);
-  };
   auto mfma_tile = [&](const bf16x8_t(&kf)[KSTEPS], f32x16_t(&acc)[2]) {
     acc[0] = f32x16_t{};
     acc[1] = f32x16_t{};
@@ -241,7 +296,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
       }
     }
   };
-  // Softmax work on a finished tile t. Only the last tile can be partial.
+  // Softmax work on the last tile t, which may be partial (exact maxima).
   auto finish_tile = [&](const f32x16_t(&acc)[2], int t, bool full) {
     if (PASS == 1) {
       // lane: window row `col` of block b; keys t*TILE + kg*32 + 8*(j/4) + 4*hf + (j%4)
@@ -277,90 +332,134 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
       red[(t & 1) * kThreads + tid] = (p4[0] + p4[1]) + (p4[2] + p4[3]);
     }
   };
-  // One pipelined iteration on full tiles: the 2*KSTEPS MFMAs of tile t+1 are
-  // interleaved one by one with slices of the softmax work of tile t (two
-  // elements per slice), fenced so that the compiler keeps the order and the
-  // matrix core and the VALU of this wave run side by side.
-  auto body = [&](int t, f32x16_t(&cur)[2], f32x16_t(&nxt)[2], bf16x8_t(&kf)[KSTEPS]) {
-    static_assert(2 * KSTEPS * 2 == 32 || 2 * KSTEPS * 4 == 32, "slices cover 32 elements");
+
+  // One pipelined iteration on full tiles, ring slot i = t % NBUF: the
+  // 2*KSTEPS MFMAs of tile t+1 are interleaved one by one with slices of the
+  // softmax work of tile t (two elements per slice at D = 128), fenced so
+  // that the matrix core and the VALU of this wave run side by side. Each
+  // k-step waits only for its own K fragment. In pass 2 one wave per tile
+  // (rotating) sums the column partials of tile t-1: its LDS reads are issued
+  // first and consumed last.
+  auto body = [&](auto ic, int t, f32x16_t(&cur)[2], f32x16_t(&nxt)[2]) {
+    constexpr int i = decltype(ic)::value;
     constexpr int PER = 32 / (2 * KSTEPS);  // elements of `cur` per MFMA
-    wait_tiles<NLD, NBUF - 2>(min(NBUF - 2, ntiles - 2 - t));  // tile t+1 has landed
+    static_assert(PER * 2 * KSTEPS == 32, "slices cover 32 elements");
+    // tile t+1 has landed; the tiles issued after it may still be in flight
+    wait_tiles<NLD, NBUF - 2>(min(NBUF - 2, ntiles - 2 - t));
     lds_barrier();
-    if (t + NBUF < ntiles) issue_tile(t + NBUF);
-    if (PASS == 2 && t > 0) reduce_tile(t - 1);
-    const uint32_t tb = kbuf_lds + ((t + 1) % NBUF) * TILE_BYTES;
+    if (t + NBUF < ntiles) issue_tile(t + NBUF, ic);  // into the slot tile t has left
+    const int rtid = (tid + 64 * i) & (kThreads - 1);
+    float part[2 * RG];
+    if (PASS == 2 && t > 0 && rtid < TILE) {
+      const int kg2 = rtid >> 5, col2 = rtid & 31;
+      const float* rp = red + ((t - 1) & 1) * kThreads;
 #pragma unroll
-    for (int st = 0; st < KSTEPS; ++st)
-      kf[st] = lds_read_b128(tb + tile_offset<D>(kr, (D / 16) * hf + st));
-    // pass 1: the tile's row maxima and the rescale factors, while LDS reads fly
-    float mnew[2], fsc[2];
-    if (PASS == 1) {
-#pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        float tmax = cur[b][0];
-#pragma unroll
-        for (int j = 1; j < 16; ++j) tmax = fmaxf(tmax, cur[b][j]);
-        mnew[b] = fmaxf(m2[b], tmax * a.c);
-        fsc[b] = fast_exp2(m2[b] - mnew[b]);
+      for (int r2 = 0; r2 < RG; ++r2) {
+        part[2 * r2] = rp[(kg2 * RG + r2) * 64 + col2];
+        part[2 * r2 + 1] = rp[(kg2 * RG + r2) * 64 + 32 + col2];
       }
     }
+    bf16x8_t kf[KSTEPS];
+    read_frags(std::integral_constant<int, (i + 1) % NBUF>{}, kf);
     __builtin_amdgcn_sched_barrier(0);
-    lds_settle(kf);
     nxt[0] = f32x16_t{};
     nxt[1] = f32x16_t{};
-    float p4[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-    for (int i = 0; i < 2 * KSTEPS; ++i) {
-      const int st = i >> 1, b = i & 1;
+    float p4[2][4];
+    static_for<0, 2 * KSTEPS>([&](auto i2c) {
+      constexpr int i2 = decltype(i2c)::value;
+      constexpr int st = i2 >> 1, b = i2 & 1;
+      if constexpr (b == 0) lds_wait<KSTEPS - 1 - st>(kf[st]);
       if (PASS == 1)
         nxt[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qf[b][st], nxt[b], 0, 0, 0);
       else
         nxt[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[b][st], kf[st], nxt[b], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int e = i * PER; e < (i + 1) * PER; ++e) {
+      for (int e = i2 * PER; e < (i2 + 1) * PER; ++e) {
         const int bb = e >> 4, j = e & 15;
-        const float ref = PASS == 1 ? mnew[bb] : lr[bb][j];
-        p4[bb][j & 3] += fast_exp2(fmaf(cur[bb][j], a.c, -ref));
+        const float ref = PASS == 1 ? m2[bb] : lr[bb][j];
+        const float p = fast_exp2(fmaf(cur[bb][j], a.c, -ref));
+        p4[bb][j & 3] = j < 4 ? p : p4[bb][j & 3] + p;  // first touch needs no add
       }
       __builtin_amdgcn_sched_barrier(0);
-    }
+    });
     if (PASS == 1) {
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
-        // full tile: mnew is finite; fsc = 0 on the first tile (m2 = -inf)
         const float sum = (p4[b][0] + p4[b][1]) + (p4[b][2] + p4[b][3]);
-        zs[b] = fmaf(zs[b], fsc[b], sum);
-        m2[b] = mnew[b];
+        const float nz = zs[b] + sum;
+        if (nz <= 0x1p64f) {  // keeps every later merge of (m2, zs) pairs finite
+          zs[b] = nz;
+        } else {  // too large (or not finite) under the current reference: move it to this tile's max
+          float tmax = cur[b][0];
+#pragma unroll
+          for (int j = 1; j < 16; ++j) tmax = fmaxf(tmax, cur[b][j]);
+          const float mnew = fmaxf(m2[b], tmax * a.c);
+          float q4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int j = 0; j < 16; ++j) q4[j & 3] += fast_exp2(fmaf(cur[b][j], a.c, -mnew));
+          zs[b] = fmaf(zs[b], fast_exp2(m2[b] - mnew), (q4[0] + q4[1]) + (q4[2] + q4[3]));
+          m2[b] = mnew;
+        }
         settle(zs[b]);  // keeps this iteration's VALU work inside this iteration
       }
     } else {
       red[(t & 1) * kThreads + tid] =
           ((p4[0][0] + p4[0][1]) + (p4[0][2] + p4[0][3])) +
           ((p4[1][0] + p4[1][1]) + (p4[1][2] + p4[1][3]));
+      if (t > 0 && rtid < TILE) {  // tile t-1 is full: only the last tile can be partial
+#pragma unroll
+        for (int k2 = 0; k2 < 2 * RG; ++k2) settle(part[k2]);  // consume the reads here, late
+        float sum = part[0];
+#pragma unroll
+        for (int k2 = 1; k2 < 2 * RG; ++k2) sum += part[k2];
+        a.sal[(size_t)lh * a.ntot + seq0 + key0 + (t - 1) * TILE + rtid] = sum;
+      }
     }
   };
 
-#pragma unroll
-  for (int t = 0; t < NBUF - 1; ++t)
-    if (t < ntiles) issue_tile(t);
+  static_for<0, NBUF - 1>([&](auto ic) {
+    if (decltype(ic)::value < ntiles) issue_tile(decltype(ic)::value, ic);
+  });
   wait_tiles<NLD, NBUF - 2>(min(NBUF - 2, ntiles - 1));  // tile 0 has landed
   lds_barrier();
-  if (NBUF - 1 < ntiles) issue_tile(NBUF - 1);
-  bf16x8_t kf[KSTEPS];
+  if (NBUF - 1 < ntiles) issue_tile(NBUF - 1, std::integral_constant<int, NBUF - 1>{});
   f32x16_t acc_a[2], acc_b[2];
-  read_frags(0, kf);
-  mfma_tile(kf, acc_a);
+  {
+    bf16x8_t kf[KSTEPS];
+    read_frags(std::integral_constant<int, 0>{}, kf);
+    lds_settle(kf);
+    mfma_tile(kf, acc_a);
+  }
+  if (PASS == 1 && ntiles > 1) {  // tile 0 is full: its maxima are the first references
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      float tmax = acc_a[b][0];
+#pragma unroll
+      for (int j = 1; j < 16; ++j) tmax = fmaxf(tmax, acc_a[b][j]);
+      m2[b] = tmax * a.c;
+    }
+  }
   int t = 0;
-  for (; t + 2 < ntiles; t += 2) {  // ping-pong accumulators, no register copies
-    body(t, acc_a, acc_b, kf);
-    body(t + 1, acc_b, acc_a, kf);
+  for (; t + NBUF < ntiles; t += NBUF) {  // ping-pong accumulators, no register copies
+    static_for<0, NBUF>([&](auto ic) {
+      if constexpr (decltype(ic)::value % 2 == 0)
+        body(ic, t + decltype(ic)::value, acc_a, acc_b);
+      else
+        body(ic, t + decltype(ic)::value, acc_b, acc_a);
+    });
   }
-  f32x16_t(&last)[2] = (t + 1 < ntiles) ? acc_b : acc_a;
-  if (t + 1 < ntiles) {
-    body(t, acc_a, acc_b, kf);
-    ++t;
-  }
+  const int rest = ntiles - 1 - t;  // 0 .. NBUF-1 full tiles before the last one
+  static_for<0, NBUF - 1>([&](auto ic) {
+    if (decltype(ic)::value < rest) {
+      if constexpr (decltype(ic)::value % 2 == 0)
+        body(ic, t + decltype(ic)::value, acc_a, acc_b);
+      else
+        body(ic, t + decltype(ic)::value, acc_b, acc_a);
+    }
+  });
+  t += rest;
+  f32x16_t(&last)[2] = (rest & 1) ? acc_b : acc_a;
   // t = ntiles - 1: the last, possibly partial, tile
   lds_barrier();
   if (PASS == 2 && t > 0) reduce_tile(t - 1);

@@ -66,6 +66,39 @@ def test_scores_and_saliency_match_oracle(cid):
             assert abs(A[l, h, a:b].sum() - w.window * w.group) < 1e-3 * w.window * w.group
 
 
+def test_saliency_with_logit_spikes_matches_oracle():
+    """Keys planted late in a key chunk lift one window row's logit by about
+    40 and 90 nats above the rest of the row: the first exceeds fp32 exp range
+    relative to the chunk's first tile, so the row's running reference has to
+    move; the second stays in range and leaves a large running sum."""
+    from synth.workloads import bf16_bits_to_f32, f32_to_bf16_bits
+
+    w = reduced("l1_8k", seqlens=[5000])
+    q = bf16_bits_to_f32(w.q_win)  # [L][S][W][Hq][d]
+    k = w.k.copy()
+    G = w.group
+    plants = []  # (kv head, key, window row, factor)
+    for h in range(w.num_kv_heads):
+        for n, (key, factor) in enumerate([(1000, 8.0), (2100, 3.5), (4500, 8.0), (4999, 8.0)]):
+            wr, g = (7 * h + 5 * n) % w.window, (h + n) % G
+            k[0, h, key] = f32_to_bf16_bits(factor * q[0, 0, wr, h * G + g])
+            plants.append((h, key, wr * G + g, factor))
+    w.k = k
+    g = GpuRun(w)
+    sc = g.score(want_saliency=True)
+    import torch
+
+    torch.cuda.synchronize()
+    o = run_oracle(w, g.budget, g.params)
+    A = sc["saliency"].cpu().numpy()
+    P = sc["scores"].cpu().numpy()
+    for h in range(w.num_kv_heads):
+        close(A[0, h], o["A"][(0, 0, h)], f"A(0,0,{h}) with spikes")
+        close(P[0, h], o["P"][(0, 0, h)], f"P(0,0,{h}) with spikes")
+    for h, key, row, factor in plants:  # each spike takes almost all of its row's mass
+        assert o["A"][(0, 0, h)][key] > 0.99, (h, key, row, factor)
+
+
 @pytest.mark.parametrize("cid", list(CASES))
 def test_step_statistics_match_oracle(cid):
     from paper_2609_22158_amd import binding as B
