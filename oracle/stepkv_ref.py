@@ -14,7 +14,13 @@ attention-based saliency, Sec. 5.2):
 * z[r, i] = scale * q_r . k_i for the window rows r = (w, g), w in [0, W),
   g in [0, G), query head h*G + g; every cached key i of the sequence is
   visible to every window row (no causal mask); scale = 1/sqrt(d).
-* A[i] = sum over rows r of the row-softmax of z (sum, not mean).
+  With causal_tail, window slot w is instead the query at position
+  N - W + w of the sequence and sees keys 0 .. N - W + w only, as in the
+  causal attention of the observation prefill that collects T_i (App. C.2);
+  a row that sees no key contributes nothing.
+* A[i] = sum over rows r of the row-softmax of z (sum, not mean). Given each
+  row's log-sum-exp lse_r over its visible keys (which the prefill's
+  attention produces), the same A[i] is sum_r exp(z[r, i] - lse_r).
 * T = 1-D average pool of A restricted to prunable tokens: window k (odd),
   stride 1, zero padding, divisor k, never crossing the sequence ends;
   protected tokens contribute zero.
@@ -48,8 +54,11 @@ __all__ = [
     "run_step_updates",
     "budget_from_ratio",
     "window_rows",
+    "visible_keys",
     "window_attention",
+    "window_row_lse",
     "window_saliency",
+    "window_saliency_from_lse",
     "pooled_saliency",
     "normalised_saliency",
     "priority",
@@ -78,6 +87,7 @@ class Params:
     r_max: float = 2.0
     s_max: float = 8.0
     eta: float = 1.5
+    causal_tail: bool = False  # window slot w sees only keys 0 .. N - W + w
 
 
 def decode_bf16(bits: np.ndarray) -> np.ndarray:
@@ -140,19 +150,70 @@ def window_rows(q_win_ls: np.ndarray, h: int, group: int) -> np.ndarray:
     return q_win_ls[:, h * group:(h + 1) * group, :].reshape(W * group, d)
 
 
-def window_attention(q_rows: np.ndarray, keys: np.ndarray, scale: float) -> np.ndarray:
-    """Row-softmax of z = scale * Q K^T over all keys: p[r, i] (fp64)."""
+def visible_keys(n_keys: int, window: int, group: int, causal_tail: bool) -> np.ndarray:
+    """Boolean [W*G][N]: whether key i is visible to window row r = w*G + g.
+
+    Without causal_tail every key is visible. With it, window slot w is the
+    query at position N - W + w and sees keys 0 .. N - W + w (causal prefill).
+    """
+    rows = window * group
+    if not causal_tail:
+        return np.ones((rows, n_keys), dtype=bool)
+    w = np.arange(rows) // group
+    return np.arange(n_keys)[None, :] <= (n_keys - window + w)[:, None]
+
+
+def _logits(q_rows: np.ndarray, keys: np.ndarray, scale: float,
+            visible: Optional[np.ndarray]) -> np.ndarray:
     z = (q_rows @ keys.T) * scale
-    m = z.max(axis=1, keepdims=True)
-    e = np.exp(z - m)
-    return e / e.sum(axis=1, keepdims=True)
+    return z if visible is None else np.where(visible, z, -np.inf)
 
 
-def window_saliency(q_rows: np.ndarray, keys: np.ndarray, scale: float) -> np.ndarray:
-    """A[i] = sum over window rows of the attention row-softmax (sums to W*G)."""
+def window_attention(q_rows: np.ndarray, keys: np.ndarray, scale: float,
+                     visible: Optional[np.ndarray] = None) -> np.ndarray:
+    """Row-softmax of z = scale * Q K^T over the visible keys: p[r, i] (fp64).
+
+    Keys a row does not see get 0; a row that sees no key is all 0.
+    """
+    z = _logits(q_rows, keys, scale, visible)
+    m = z.max(axis=1, keepdims=True) if z.shape[1] else np.full((z.shape[0], 1), -np.inf)
+    e = np.exp(z - np.where(np.isfinite(m), m, 0.0))
+    tot = e.sum(axis=1, keepdims=True)
+    return np.divide(e, tot, out=np.zeros_like(e), where=tot > 0)
+
+
+def window_row_lse(q_rows: np.ndarray, keys: np.ndarray, scale: float,
+                   visible: Optional[np.ndarray] = None) -> np.ndarray:
+    """Natural-log log-sum-exp of each window row over its visible keys (-inf if none)."""
+    z = _logits(q_rows, keys, scale, visible)
+    m = z.max(axis=1) if z.shape[1] else np.full(z.shape[0], -np.inf)
+    safe = np.where(np.isfinite(m), m, 0.0)
+    tot = np.exp(z - safe[:, None]).sum(axis=1)
+    with np.errstate(divide="ignore"):
+        return np.where(tot > 0, safe + np.log(tot), -np.inf)
+
+
+def window_saliency(q_rows: np.ndarray, keys: np.ndarray, scale: float,
+                    visible: Optional[np.ndarray] = None) -> np.ndarray:
+    """A[i] = sum over window rows of the attention row-softmax (sums to the number of
+    rows that see at least one key: W*G without a causal tail)."""
     if keys.shape[0] == 0:
         return np.zeros(0)
-    return window_attention(q_rows, keys, scale).sum(axis=0)
+    return window_attention(q_rows, keys, scale, visible).sum(axis=0)
+
+
+def window_saliency_from_lse(q_rows: np.ndarray, keys: np.ndarray, scale: float,
+                             lse: np.ndarray, visible: Optional[np.ndarray] = None) -> np.ndarray:
+    """A[i] = sum over rows r that see key i of exp(z[r, i] - lse_r), given each row's
+    log-sum-exp lse_r (natural log) over the keys it sees (App. C.2: T_i comes out of
+    the observation prefill, whose attention already normalises every row)."""
+    if keys.shape[0] == 0:
+        return np.zeros(0)
+    z = (q_rows @ keys.T) * scale
+    vis = np.ones(z.shape, dtype=bool) if visible is None else visible
+    lse = np.asarray(lse, dtype=np.float64)[:, None]
+    arg = np.where(vis, z - np.where(np.isfinite(lse), lse, 0.0), -np.inf)
+    return np.exp(arg).sum(axis=0)
 
 
 def pooled_saliency(A: np.ndarray, prunable: np.ndarray, k: int) -> np.ndarray:
@@ -253,9 +314,19 @@ def decode_attention(q: np.ndarray, K: np.ndarray, V: np.ndarray, scale: float) 
 
 # ------------------------------------------------------------- whole pass
 def score_head(q_rows: np.ndarray, keys: np.ndarray, step_ids: np.ndarray,
-               prunable: np.ndarray, S: np.ndarray, p: Params, scale: float):
-    """Saliency, pooling, normalisation and priority for one (sequence, layer, KV head)."""
-    A = window_saliency(q_rows, keys, scale)
+               prunable: np.ndarray, S: np.ndarray, p: Params, scale: float,
+               window: Optional[int] = None, lse: Optional[np.ndarray] = None):
+    """Saliency, pooling, normalisation and priority for one (sequence, layer, KV head).
+
+    window (W) is needed with p.causal_tail; lse (per window row, natural log)
+    selects the saliency from given log-sum-exps."""
+    visible = None
+    if p.causal_tail:
+        visible = visible_keys(keys.shape[0], window, q_rows.shape[0] // window, True)
+    if lse is None:
+        A = window_saliency(q_rows, keys, scale, visible)
+    else:
+        A = window_saliency_from_lse(q_rows, keys, scale, lse, visible)
     T = pooled_saliency(A, prunable, p.pool_kernel)
     T_hat = normalised_saliency(T, prunable)
     P = priority(T_hat, step_ids, S, prunable, p.alpha, p.beta)
@@ -266,12 +337,15 @@ def compress(q_win: np.ndarray, k: np.ndarray, v: Optional[np.ndarray], cu_seqle
              step_ids: np.ndarray, protected: np.ndarray, cu_steps: np.ndarray,
              S: np.ndarray, budget: int, p: Params = Params(),
              layers: Optional[Sequence[int]] = None, heads: Optional[Sequence[int]] = None,
-             seqs: Optional[Sequence[int]] = None, want_saliency: bool = False) -> Dict:
+             seqs: Optional[Sequence[int]] = None, want_saliency: bool = False,
+             lse_win: Optional[np.ndarray] = None) -> Dict:
     """Run the pass over the chosen (sequence, layer, KV head) triples, one at a time.
 
     Arguments use the library's layouts with bf16 as uint16 bits:
     q_win [L][S][W][Hq][d], k/v [L][Hkv][Ntot][d], step_ids/protected [Ntot],
-    S [cu_steps[-1]] (fp64 step utilities). Results are keyed by (s, l, h).
+    S [cu_steps[-1]] (fp64 step utilities), and optionally lse_win [L][S][W][Hq],
+    the window rows' natural-log log-sum-exps to take the saliency from.
+    Results are keyed by (s, l, h).
     """
     L, nseq, W, Hq, d = q_win.shape
     Hkv = k.shape[1]
@@ -288,7 +362,12 @@ def compress(q_win: np.ndarray, k: np.ndarray, v: Optional[np.ndarray], cu_seqle
             qs = decode_bf16(q_win[l, s])
             for h in (range(Hkv) if heads is None else heads):
                 keys = decode_bf16(k[l, h, a:b])
-                A, T_hat, P = score_head(window_rows(qs, h, G), keys, sid, prun, Ss, p, scale)
+                lse = None
+                if lse_win is not None:
+                    lse = np.asarray(lse_win[l, s][:, h * G:(h + 1) * G],
+                                     dtype=np.float64).reshape(W * G)
+                A, T_hat, P = score_head(window_rows(qs, h, G), keys, sid, prun, Ss, p, scale,
+                                         window=W, lse=lse)
                 idx = select_retained(P, prun, budget)
                 key = (s, l, h)
                 out["P"][key] = P

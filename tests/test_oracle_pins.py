@@ -147,6 +147,106 @@ def test_saliency_brute_force_loops():
     np.testing.assert_allclose(O.window_saliency(q, k, scale), A, rtol=1e-12)
 
 
+# ------------------------------------------------------------- causal tail, saliency from LSE
+def test_causal_visibility_rule():
+    """Window slot w is the query at position N - W + w and sees keys 0 .. N - W + w."""
+    vis = O.visible_keys(10, 4, 2, True)
+    assert vis.shape == (8, 10)
+    for r in range(8):
+        w = r // 2
+        assert vis[r].tolist() == [i <= 10 - 4 + w for i in range(10)]
+    assert O.visible_keys(10, 4, 2, False).all()
+
+
+def test_causal_saliency_brute_force_loops():
+    """Pure-Python loops with math.exp over each row's visible keys only."""
+    W, G, d, n = 4, 2, 64, 23
+    q, k = _rows_keys(W, G, d, n, 5)
+    scale = 0.125
+    A = [0.0] * n
+    for r in range(W * G):
+        w = r // G
+        seen = [i for i in range(n) if i <= n - W + w]
+        z = {i: scale * sum(q[r, j] * k[i, j] for j in range(d)) for i in seen}
+        m = max(z.values())
+        t = sum(math.exp(x - m) for x in z.values())
+        for i in seen:
+            A[i] += math.exp(z[i] - m) / t
+    got = O.window_saliency(q, k, scale, O.visible_keys(n, W, G, True))
+    np.testing.assert_allclose(got, A, rtol=1e-12)
+
+
+def test_causal_single_slot_sees_everything():
+    """W = 1: the last query sees every key, so the causal tail changes nothing."""
+    q, k = _rows_keys(1, 4, 128, 77, 6)
+    scale = 1.0 / math.sqrt(128)
+    np.testing.assert_allclose(O.window_saliency(q, k, scale, O.visible_keys(77, 1, 4, True)),
+                               O.window_saliency(q, k, scale), rtol=1e-14)
+
+
+def test_causal_full_window_is_causal_attention():
+    """N = W, G = 1: column sums of a lower-triangular softmax (torch masked softmax)."""
+    n = 19
+    q, k = _rows_keys(n, 1, 64, n, 7)
+    scale = 0.125
+    z = torch.from_numpy((q @ k.T) * scale)
+    z = z.masked_fill(torch.triu(torch.ones(n, n, dtype=torch.bool), diagonal=1), -math.inf)
+    ref = torch.softmax(z, dim=1).sum(dim=0).numpy()
+    got = O.window_saliency(q, k, scale, O.visible_keys(n, n, 1, True))
+    np.testing.assert_allclose(got, ref, rtol=1e-12)
+    assert abs(got[-1] - float(torch.softmax(z, dim=1)[-1, -1])) < 1e-14  # only the last row sees it
+
+
+def test_causal_rows_without_keys_contribute_nothing():
+    """N < W: slots w < W - N see no key; the sum of A counts only the other N*G rows."""
+    W, G, n = 8, 2, 5
+    q, k = _rows_keys(W, G, 64, n, 8)
+    vis = O.visible_keys(n, W, G, True)
+    assert (~vis[: (W - n) * G]).all() and vis[(W - n) * G:].any(axis=1).all()
+    A = O.window_saliency(q, k, 0.125, vis)
+    assert abs(A.sum() - n * G) < 1e-12
+    lse = O.window_row_lse(q, k, 0.125, vis)
+    assert np.isneginf(lse[: (W - n) * G]).all() and np.isfinite(lse[(W - n) * G:]).all()
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_row_lse_matches_scipy_logsumexp(causal):
+    """Row log-sum-exp over the visible keys equals scipy's logsumexp on the same logits."""
+    W, G, n = 16, 4, 300
+    q, k = _rows_keys(W, G, 128, n, 9)
+    scale = 1.0 / math.sqrt(128)
+    vis = O.visible_keys(n, W, G, causal)
+    z = (q @ k.T) * scale
+    ref = np.array([scipy.special.logsumexp(z[r][vis[r]]) for r in range(W * G)])
+    np.testing.assert_allclose(O.window_row_lse(q, k, scale, vis), ref, rtol=1e-13)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_saliency_from_exact_lse_equals_softmax_sums(causal):
+    """Fed the exact row LSE (from scipy), the one-sweep form gives the two-sweep A."""
+    W, G, n = 16, 4, 300
+    q, k = _rows_keys(W, G, 128, n, 10)
+    scale = 1.0 / math.sqrt(128)
+    vis = O.visible_keys(n, W, G, causal)
+    z = (q @ k.T) * scale
+    lse = np.array([scipy.special.logsumexp(z[r][vis[r]]) for r in range(W * G)])
+    ref = scipy.special.softmax(np.where(vis, z, -np.inf), axis=1).sum(axis=0)
+    np.testing.assert_allclose(O.window_saliency_from_lse(q, k, scale, lse, vis), ref, rtol=1e-12)
+    np.testing.assert_allclose(O.window_saliency(q, k, scale, vis), ref, rtol=1e-12)
+
+
+def test_saliency_from_lse_shift():
+    """Raising row r's LSE by delta_r scales that row's contribution by exp(-delta_r)."""
+    W, G, n = 8, 2, 120
+    q, k = _rows_keys(W, G, 64, n, 11)
+    scale = 0.125
+    lse = O.window_row_lse(q, k, scale)
+    delta = np.linspace(-2.0, 3.0, W * G)
+    p = O.window_attention(q, k, scale)
+    np.testing.assert_allclose(O.window_saliency_from_lse(q, k, scale, lse + delta),
+                               (p * np.exp(-delta)[:, None]).sum(axis=0), rtol=1e-12)
+
+
 # ------------------------------------------------------------- pooling, normalisation
 def test_pool_constant_closed_form():
     """Constant A on prunable tokens: interior T = A, an edge with e missing taps gives A(k-e)/k."""
