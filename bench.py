@@ -6,7 +6,12 @@ One step = the whole pass over one synthetic batch: host step-utility update
 compaction, all layers and KV heads. Inputs are resident in HBM before the
 timed region. Prints one JSON line.
 
-    python bench.py [--steps K] [--warmup W] [--workload l32_32k] [--budget 1024]
+By default the saliency is computed from the window queries and the cache
+alone (two sweeps over K). With --lse-fed the window rows' log-sum-exps are
+an input, as the observation prefill's attention provides them (App. C.2),
+and the saliency takes one sweep.
+
+    python bench.py [--steps K] [--warmup W] [--workload l32_32k] [--budget 1024] [--lse-fed]
 """
 from __future__ import annotations
 
@@ -41,6 +46,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget for the oracle CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--lse-fed", action="store_true",
+                    help="take the window rows' log-sum-exps as an input (one sweep over K)")
+    ap.add_argument("--causal-tail", action="store_true",
+                    help="window slot w sees keys up to N - W + w only (causal prefill)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this size (HBM counter calibration)")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -49,7 +58,19 @@ def parse():
     return ap.parse_args()
 
 
-SALIENCY_KERNELS = ("saliency_kernel", "lse_combine_kernel", "chunk_plan_kernel")
+SALIENCY_KERNELS = ("saliency_kernel", "lse_combine_kernel", "lse_import_kernel",
+                    "chunk_plan_kernel")
+
+
+def _saliency_part(name: str, lse_fed: bool):
+    """The saliency-stage kernel a dispatch belongs to, or None. With lse_fed the
+    row-LSE sweep and its combine belong to the untimed prefill stand-in."""
+    for k in SALIENCY_KERNELS:
+        if k in name:
+            if lse_fed and (k == "lse_combine_kernel" or (k == "saliency_kernel" and ", 1>" in name)):
+                return None
+            return k
+    return None
 
 
 def record_traffic(args) -> None:
@@ -77,16 +98,18 @@ def record_traffic(args) -> None:
         copies = [d for d in vals if "copyBuffer" in names[d]]
         cal = probe / (max(vals[d] for d in copies) * 1024.0)  # bytes per counted byte
         per_kernel = defaultdict(list)
+        plans = sorted((int(d) for d in vals if "chunk_plan_kernel" in names[d]))
         for d, v in vals.items():
-            for k in SALIENCY_KERNELS:
-                if k in names[d]:
-                    per_kernel[k].append(v * 1024.0 * cal)
+            k = _saliency_part(names[d], args.lse_fed)
+            if k is None or (args.lse_fed and k == "chunk_plan_kernel" and int(d) == plans[0]):
+                continue  # the first plan of an LSE-fed run belongs to the untimed row-LSE call
+            per_kernel[k].append(v * 1024.0 * cal)
         launches = len(per_kernel["chunk_plan_kernel"])  # one per saliency launch
         out[counter] = {"calibration": cal, "launches": launches,
                         "bytes": sum(sum(v) for v in per_kernel.values()) / launches,
                         "per_kernel": {k: sum(v) / launches for k, v in per_kernel.items()}}
     budget = args.budget or 1024
-    key = f"{args.workload}_b{budget}_w{args.window or 64}"
+    key = traffic_key(args.workload, budget, args.window or 64, args.lse_fed)
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         db = json.load(open(path))
@@ -117,12 +140,16 @@ def source_digest() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def recorded_traffic(workload: str, budget: int, window: int):
+def traffic_key(workload: str, budget: int, window: int, lse_fed: bool) -> str:
+    return f"{workload}_b{budget}_w{window}" + ("_lse" if lse_fed else "")
+
+
+def recorded_traffic(key: str):
     """HBM bytes per saliency launch from the committed counter runs, or None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as f:
-            rec = json.load(f).get(f"{workload}_b{budget}_w{window}")
+            rec = json.load(f).get(key)
     except (OSError, ValueError):
         return None
     if not rec or rec.get("saliency_source_sha256") != source_digest():
@@ -130,8 +157,11 @@ def recorded_traffic(workload: str, budget: int, window: int):
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, budget, seconds):
-    """Time the oracle on whole (sequence, layer, KV head) triples until `seconds` pass."""
+def cpu_baseline(w, budget, seconds, params, lse_fed=False):
+    """Time the oracle on whole (sequence, layer, KV head) triples until `seconds` pass.
+
+    With lse_fed the oracle takes each triple's row log-sum-exps as given (computed
+    beforehand by the oracle itself, outside the timed region)."""
     import oracle as O
 
     try:
@@ -146,15 +176,26 @@ def cpu_baseline(w, budget, seconds):
                for s in range(w.num_seqs)]
     rng = np.random.default_rng(0)
     rng.shuffle(triples)
-    done, tokens, t0 = 0, 0, time.perf_counter()
+    op = O.Params(causal_tail=bool(params.causal_tail))
+    G = w.num_q_heads // w.num_kv_heads
+    lse_win = np.zeros(w.q_win.shape[:4]) if lse_fed else None
+    done, tokens, dt = 0, 0, 0.0
     for s, l, h in triples:
+        if lse_fed:  # the prefill's output, not part of the timed work
+            a, b = int(w.cu_seqlens[s]), int(w.cu_seqlens[s + 1])
+            rows = O.window_rows(O.decode_bf16(w.q_win[l, s]), h, G)
+            vis = O.visible_keys(b - a, w.window, G, op.causal_tail)
+            lse = O.window_row_lse(rows, O.decode_bf16(w.k[l, h, a:b]),
+                                   1.0 / math.sqrt(w.head_dim), vis)
+            lse_win[l, s, :, h * G:(h + 1) * G] = lse.reshape(w.window, G)
+        t0 = time.perf_counter()
         O.compress(w.q_win, w.k, w.v, w.cu_seqlens, w.step_ids, w.protected, w.cu_steps, S,
-                   budget, O.Params(), layers=[l], heads=[h], seqs=[s])
+                   budget, op, layers=[l], heads=[h], seqs=[s], lse_win=lse_win)
+        dt += time.perf_counter() - t0
         done += 1
         tokens += w.seqlens[s]
-        if time.perf_counter() - t0 >= seconds:
+        if dt >= seconds:
             break
-    dt = time.perf_counter() - t0
     # whole-job rate: every token is scored in all L x Hkv heads
     per_head_rate = tokens / dt
     value = per_head_rate / (w.num_layers * w.num_kv_heads)
@@ -210,8 +251,12 @@ def main():
     k_out = torch.empty((L, Hkv, out_rows, d), dtype=torch.bfloat16, device=dev)
     v_out = torch.empty_like(k_out)
     ws = torch.empty(pb.saliency_workspace_bytes(), dtype=torch.uint8, device=dev)
-    params = B.Params()
+    params = B.Params(causal_tail=int(args.causal_tail))
     stream = torch.cuda.current_stream()
+    lse = None
+    if args.lse_fed:  # stands for the prefill attention's row LSE, resident in HBM
+        lse = B.window_lse(pb, q, k, params, workspace=ws)
+        torch.cuda.synchronize()
 
     def step(ev=None):
         # a0: host step utility (Algorithm 1 phases 1-2) for every sequence
@@ -221,7 +266,10 @@ def main():
         util.copy_(util_pinned, non_blocking=True)
         if ev:
             ev[0].record(stream)
-        B.saliency(pb, q, k, params, workspace=ws, out=sal)
+        if lse is None:
+            B.saliency(pb, q, k, params, workspace=ws, out=sal)
+        else:
+            B.saliency_from_lse(pb, q, k, lse, params, workspace=ws, out=sal)
         if ev:
             ev[1].record(stream)
         B.priority(pb, sal, sid, prot, util, params, scores=scores)
@@ -268,19 +316,30 @@ def main():
     G = w.num_q_heads // Hkv
     R = w.window * G
     lh = L * Hkv
-    # algorithmic work per launch
+    # algorithmic work per launch of the saliency stage
+    sweeps = 1 if args.lse_fed else 2
     k_bytes = lh * ntot * d * 2
-    sal_flops = 2 * 2 * R * d * ntot * lh            # two sweeps of Q K^T
+    sal_flops = sweeps * 2 * R * d * ntot * lh         # Q K^T once per sweep
     sal_bytes = k_bytes + lh * ntot * 4 + q.numel() * 2  # K once, A written, Q read
+    if args.lse_fed:
+        sal_bytes += lse.numel() * 4
     compact_bytes = lh * out_rows * d * 2 * 2 * 2     # K and V rows, read and written
     t_sal = stage_ms["saliency"] * 1e-3
     t_cmp = stage_ms["compact"] * 1e-3
     achieved_tflops = sal_flops / t_sal / 1e12
-    roofline = {"bound": "mfma", "achieved": round(achieved_tflops, 2),
-                "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved_tflops / BF16_PEAK_TFLOPS, 4),
-                "traffic": recorded_traffic(args.workload, budget, w.window),
-                "kernel": "saliency (two MFMA sweeps over K)"}
+    achieved_gbs = sal_bytes / t_sal / 1e9
+    kernel = ("saliency (one MFMA sweep over K, row LSE given)" if args.lse_fed
+              else "saliency (two MFMA sweeps over K)")
+    traffic = recorded_traffic(traffic_key(args.workload, budget, w.window, args.lse_fed))
+    # the binding roofline: whichever of HBM and MFMA needs longer at peak
+    if sal_bytes / (HBM_PEAK_GBS * 1e9) >= sal_flops / (BF16_PEAK_TFLOPS * 1e12):
+        roofline = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(achieved_gbs / HBM_PEAK_GBS, 4)}
+    else:
+        roofline = {"bound": "mfma", "achieved": round(achieved_tflops, 2),
+                    "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(achieved_tflops / BF16_PEAK_TFLOPS, 4)}
+    roofline.update({"traffic": traffic, "kernel": kernel})
     hbm = {"saliency_gbps": round(sal_bytes / t_sal / 1e9, 1),
            "saliency_frac": round(sal_bytes / t_sal / 1e9 / HBM_PEAK_GBS, 4),
            "compact_gbps": round(compact_bytes / t_cmp / 1e9, 1),
@@ -295,7 +354,10 @@ def main():
         "config": {"workload": f"{args.workload}: {L} layers, {w.num_q_heads} query / {Hkv} KV "
                                f"heads, d {d}, {w.num_seqs} sequence(s) of {w.seqlens[:4]}"
                                f"{'...' if w.num_seqs > 4 else ''} tokens, window {w.window}, "
-                               f"budget {budget} per KV head",
+                               f"budget {budget} per KV head"
+                               + (", row LSE given" if args.lse_fed else "")
+                               + (", causal window" if args.causal_tail else ""),
+                   "saliency_sweeps": sweeps, "causal_tail": bool(args.causal_tail),
                    "layers": L, "kv_heads": Hkv, "q_heads": w.num_q_heads, "head_dim": d,
                    "seq_len": int(max(w.seqlens)), "tokens": int(ntot), "window": w.window,
                    "budget": budget, "seed": args.seed},
@@ -305,7 +367,7 @@ def main():
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, budget, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(w, budget, args.cpu_seconds, params, args.lse_fed)
     print(json.dumps(line), flush=True)
 
 

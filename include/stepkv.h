@@ -12,7 +12,9 @@
  *                   retention priority P_i = alpha*T_i + beta*S_k
  *                   (Sec. 5.2, eq. token-priority); it is the composition of
  *                   stepkv_saliency (the attention sweeps over K) and
- *                   stepkv_priority (pooling, normalisation, fusion)
+ *                   stepkv_priority (pooling, normalisation, fusion).
+ *                   stepkv_score_from_lse takes the window rows' log-sum-exps
+ *                   from the caller's prefill (App. C.2) and sweeps K once.
  *   stepkv_select   global top-B ranking per (sequence, layer, KV head)
  *                   (Sec. 5.2 last paragraph; Algorithm 1 phase 3)
  *   stepkv_compact  C_hat = C_prot || C_traj[K] (eq. problem)
@@ -36,6 +38,7 @@
  * Layouts (L layers, S sequences, Hq query heads, Hkv KV heads, G = Hq/Hkv,
  * d head dim, W window length, Ntot = cu_seqlens[S]):
  *  q_win        bf16  [L][S][W][Hq][d]   last W queries of every sequence
+ *  lse_win      fp32  [L][S][W][Hq]      natural-log row log-sum-exp of them
  *  k, v         bf16  [L][Hkv][Ntot][d]  sequences concatenated along Ntot
  *  step_ids     int32 [Ntot]             step index local to the sequence
  *  protected    uint8 [Ntot]             nonzero = protected (never pruned)
@@ -100,6 +103,12 @@ typedef struct stepkv_params {
   float r_min, r_max;   /* completion-score clip (-1, 2) */
   float s_max;          /* utility clip S_max (8) */
   float eta;            /* reuse update scale (1.5) */
+  /* window visibility (0): 0 = every window row sees all N_s keys of its
+   * sequence; nonzero = window slot w is the query at position N_s - W + w
+   * and sees keys 0 .. N_s - W + w only, as in the causal attention of the
+   * observation prefill that yields T_i (App. C.2). A row that sees no key
+   * (N_s < W - w) contributes nothing. */
+  int32_t causal_tail;
 } stepkv_params;
 
 /* Per-step statistics of one (layer, KV head, step), from stepkv_score:
@@ -158,14 +167,40 @@ size_t stepkv_saliency_workspace_bytes(const stepkv_problem* pb);
 /* Sec. 5.2, token saliency: the raw observation-window saliency
  *   A_i = sum_r softmax_i(scale * q_r . k_i)
  * of every token, for every (sequence, layer, KV head), written to saliency
- * fp32 [L][Hkv][Ntot]. Window rows r = w*G + g use query head h*G + g; all
- * N_s keys of the sequence are visible. Computed exactly (two sweeps over K:
- * row log-sum-exp, then column sums), fp32 accumulation of bf16 products.
+ * fp32 [L][Hkv][Ntot]. Window rows r = w*G + g use query head h*G + g; the
+ * softmax runs over the keys each row sees (all N_s keys, or the causal tail
+ * of prm->causal_tail). Computed exactly (two sweeps over K: row
+ * log-sum-exp, then column sums), fp32 accumulation of bf16 products.
  * Errors: EINVAL (null pointers, bad problem or scale), EUNSUPPORTED (d not in
  * {64,128} or W*G > STEPKV_MAX_WINDOW_ROWS), EWORKSPACE, EHIP. */
 int stepkv_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
                     const void* k, float* saliency, void* workspace, size_t ws_bytes,
                     void* stream);
+
+/* Row log-sum-exp of the window attention (the first of the two sweeps):
+ *   lse_win[l][s][w][h*G+g] = ln sum_{i seen by row (w,g)} exp(scale * q . k_i)
+ * natural log, fp32 [L][S][W][Hq]; -inf for a row that sees no key. This is
+ * the quantity a prefill attention kernel reports per query row, so either
+ * source can feed stepkv_saliency_from_lse. Workspace and errors as
+ * stepkv_saliency. */
+int stepkv_window_lse(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                      const void* k, float* lse_win, void* workspace, size_t ws_bytes,
+                      void* stream);
+
+/* App. C.2: the token saliency collected inside the observation prefill,
+ * whose attention has already normalised every window row. Given each row's
+ * natural-log log-sum-exp lse_win fp32 [L][S][W][Hq] over the keys it sees
+ * (as stepkv_window_lse returns, or as the prefill's attention reports for
+ * the last W query positions when prm->causal_tail is set), one sweep over K
+ * gives
+ *   A_i = sum_{r seeing i} exp(scale * q_r . k_i - lse_r)
+ * written like stepkv_saliency. An lse of -inf marks a row that sees no key.
+ * The result equals stepkv_saliency's to rounding when lse_win is exact;
+ * otherwise each row's contribution scales by exp(exact - given).
+ * Workspace and errors as stepkv_saliency. */
+int stepkv_saliency_from_lse(const stepkv_problem* pb, const stepkv_params* prm,
+                             const void* q_win, const void* k, const float* lse_win,
+                             float* saliency, void* workspace, size_t ws_bytes, void* stream);
 
 /* Sec. 5.2, eq. token-priority, from a saliency computed by stepkv_saliency:
  *   T_i = (1/k) sum_{|j-i| <= k/2} A_j [j prunable], zero padding, per sequence
@@ -199,6 +234,15 @@ int stepkv_score(const stepkv_problem* pb, const stepkv_params* prm, const void*
                  const void* k, const int32_t* step_ids, const uint8_t* protected_mask,
                  const float* step_utility, float* scores, float* saliency,
                  stepkv_step_stat* step_stats, void* workspace, size_t ws_bytes, void* stream);
+
+/* stepkv_score with the saliency taken from given row log-sum-exps
+ * (stepkv_saliency_from_lse, one sweep over K) instead of both sweeps.
+ * Same outputs, workspace size and errors as stepkv_score. */
+int stepkv_score_from_lse(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                          const void* k, const float* lse_win, const int32_t* step_ids,
+                          const uint8_t* protected_mask, const float* step_utility,
+                          float* scores, float* saliency, stepkv_step_stat* step_stats,
+                          void* workspace, size_t ws_bytes, void* stream);
 
 /* Sec. 5.2 / Algorithm 1 phase 3 / eq. problem: for every (sequence, layer,
  * KV head), keep every protected token plus exactly min(B, N_pr) prunable

@@ -19,7 +19,9 @@ from .binding import (  # noqa: F401
     priority,
     retained_rows,
     saliency,
+    saliency_from_lse,
     score,
     select,
     step_utilities,
+    window_lse,
 )

@@ -54,6 +54,7 @@ class ParamsC(ctypes.Structure):
         ("r_max", ctypes.c_float),
         ("s_max", ctypes.c_float),
         ("eta", ctypes.c_float),
+        ("causal_tail", ctypes.c_int32),
     ]
 
 
@@ -89,6 +90,13 @@ _SIGNATURES = {
                                        _vp, _vp, _vp, _vp, _vp, _vp]),
     "stepkv_score": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp, _vp,
                                     _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "stepkv_window_lse": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp,
+                                         _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "stepkv_saliency_from_lse": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC),
+                                                _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "stepkv_score_from_lse": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC),
+                                             _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                             ctypes.c_size_t, _vp]),
     "stepkv_select": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, _vp, _vp, ctypes.c_int32,
                                      _vp, _vp, _vp, _vp, _vp]),
     "stepkv_compact": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, _vp, _vp, _vp,
@@ -153,6 +161,7 @@ class Params:
     r_max: float = 2.0
     s_max: float = 8.0
     eta: float = 1.5
+    causal_tail: int = 0  # nonzero: window slot w sees keys 0 .. N - W + w only
 
     def c(self) -> ParamsC:
         return ParamsC(*[getattr(self, f) for f, _ in ParamsC._fields_])
@@ -253,9 +262,13 @@ def _need(t, dtype, shape, name):
 
 
 def score(pb: Problem, q_win, k, step_ids, protected, step_utility, params: Optional[Params] = None,
-          *, want_saliency: bool = False, want_stats: bool = False, workspace=None, scores=None,
-          stream=None):
-    """stepkv_score: priorities P [L*Hkv][Ntot] (and optionally A and step stats)."""
+          *, lse=None, want_saliency: bool = False, want_stats: bool = False, workspace=None,
+          scores=None, stream=None):
+    """stepkv_score: priorities P [L*Hkv][Ntot] (and optionally A and step stats).
+
+    With `lse` (fp32 [L][S][W][Hq], the window rows' natural-log log-sum-exps)
+    this is stepkv_score_from_lse: one sweep over K instead of two.
+    """
     import torch
 
     lib = load()
@@ -263,6 +276,7 @@ def score(pb: Problem, q_win, k, step_ids, protected, step_utility, params: Opti
     dev = pb.device
     qp = _need(q_win, torch.bfloat16, (L, S, W, pb.num_q_heads, d), "q_win")
     kp = _need(k, torch.bfloat16, (L, Hkv, pb.ntot, d), "k")
+    lp = _need(lse, torch.float32, (L, S, W, pb.num_q_heads), "lse") if lse is not None else None
     sp = _need(step_ids, torch.int32, (pb.ntot,), "step_ids")
     pp = _need(protected, torch.uint8, (pb.ntot,), "protected")
     up = _need(step_utility, torch.float32, (pb.total_steps,), "step_utility")
@@ -275,11 +289,15 @@ def score(pb: Problem, q_win, k, step_ids, protected, step_utility, params: Opti
     need = pb.workspace_bytes()
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    rc = lib.stepkv_score(ctypes.byref(pb.c), ctypes.byref((params or Params()).c()), qp, kp, sp, pp,
-                          up, scores.data_ptr(), sal.data_ptr() if sal is not None else None,
-                          stats.data_ptr() if stats is not None else None, workspace.data_ptr(),
-                          workspace.numel(), _stream(stream))
-    _check("stepkv_score", rc)
+    tail = (scores.data_ptr(), sal.data_ptr() if sal is not None else None,
+            stats.data_ptr() if stats is not None else None, workspace.data_ptr(),
+            workspace.numel(), _stream(stream))
+    prm = ctypes.byref((params or Params()).c())
+    if lp is None:
+        _check("stepkv_score", lib.stepkv_score(ctypes.byref(pb.c), prm, qp, kp, sp, pp, up, *tail))
+    else:
+        _check("stepkv_score_from_lse",
+               lib.stepkv_score_from_lse(ctypes.byref(pb.c), prm, qp, kp, lp, sp, pp, up, *tail))
     if sal is not None:
         out["saliency"] = sal
     if stats is not None:
@@ -306,6 +324,50 @@ def saliency(pb: Problem, q_win, k, params: Optional[Params] = None, *, workspac
                              out.data_ptr(), workspace.data_ptr(), workspace.numel(),
                              _stream(stream))
     _check("stepkv_saliency", rc)
+    return out
+
+
+def window_lse(pb: Problem, q_win, k, params: Optional[Params] = None, *, workspace=None,
+               out=None, stream=None):
+    """stepkv_window_lse: natural-log row log-sum-exp of the window attention, [L][S][W][Hq]."""
+    import torch
+
+    lib = load()
+    L, Hkv, d, W, S = pb.num_layers, pb.num_kv_heads, pb.head_dim, pb.window, pb.num_seqs
+    qp = _need(q_win, torch.bfloat16, (L, S, W, pb.num_q_heads, d), "q_win")
+    kp = _need(k, torch.bfloat16, (L, Hkv, pb.ntot, d), "k")
+    if out is None:
+        out = torch.empty((L, S, W, pb.num_q_heads), dtype=torch.float32, device=pb.device)
+    op = _need(out, torch.float32, (L, S, W, pb.num_q_heads), "lse")
+    if workspace is None:
+        workspace = torch.empty(max(pb.saliency_workspace_bytes(), 1), dtype=torch.uint8,
+                                device=pb.device)
+    rc = lib.stepkv_window_lse(ctypes.byref(pb.c), ctypes.byref((params or Params()).c()), qp, kp,
+                               op, workspace.data_ptr(), workspace.numel(), _stream(stream))
+    _check("stepkv_window_lse", rc)
+    return out
+
+
+def saliency_from_lse(pb: Problem, q_win, k, lse, params: Optional[Params] = None, *,
+                      workspace=None, out=None, stream=None):
+    """stepkv_saliency_from_lse: A [L][Hkv][Ntot] in one sweep, given the rows' LSE."""
+    import torch
+
+    lib = load()
+    L, Hkv, d, W, S = pb.num_layers, pb.num_kv_heads, pb.head_dim, pb.window, pb.num_seqs
+    qp = _need(q_win, torch.bfloat16, (L, S, W, pb.num_q_heads, d), "q_win")
+    kp = _need(k, torch.bfloat16, (L, Hkv, pb.ntot, d), "k")
+    lp = _need(lse, torch.float32, (L, S, W, pb.num_q_heads), "lse")
+    if out is None:
+        out = torch.empty((L, Hkv, pb.ntot), dtype=torch.float32, device=pb.device)
+    _need(out, torch.float32, (L, Hkv, pb.ntot), "saliency")
+    if workspace is None:
+        workspace = torch.empty(max(pb.saliency_workspace_bytes(), 1), dtype=torch.uint8,
+                                device=pb.device)
+    rc = lib.stepkv_saliency_from_lse(ctypes.byref(pb.c), ctypes.byref((params or Params()).c()),
+                                      qp, kp, lp, out.data_ptr(), workspace.data_ptr(),
+                                      workspace.numel(), _stream(stream))
+    _check("stepkv_saliency_from_lse", rc)
     return out
 
 

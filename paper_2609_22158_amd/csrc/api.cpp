@@ -130,6 +130,7 @@ void stepkv_params_default(stepkv_params* p) {
   p->r_max = 2.0f;
   p->s_max = 8.0f;
   p->eta = 1.5f;
+  p->causal_tail = 0;
 }
 
 const char* stepkv_strerror(int code) {
@@ -202,9 +203,12 @@ int max_steps_per_seq(const stepkv_problem* pb) {
   return m;
 }
 
-// Saliency sweeps into `sal`, using workspace regions below layout().sal.
+// Saliency sweeps into `sal` (or the row LSE into lse_out, or from lse_in),
+// using workspace regions below layout().sal.
 int run_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
-                 const void* k, float* sal, uint8_t* ws, hipStream_t st) {
+                 const void* k, float* sal, uint8_t* ws, hipStream_t st,
+                 SaliencyMode mode = SaliencyMode::kBoth, const float* lse_in = nullptr,
+                 float* lse_out = nullptr) {
   const SaliencyPlan plan = plan_saliency(pb);
   const WsLayout w = layout(pb, plan);
   const int d = pb->head_dim;
@@ -216,6 +220,9 @@ int run_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void*
   sa.partial = reinterpret_cast<float2*>(ws + w.partial);
   sa.lse2 = reinterpret_cast<float*>(ws + w.lse);
   sa.sal = sal;
+  sa.lse_in = lse_in;
+  sa.lse_out = lse_out;
+  sa.causal = prm->causal_tail != 0;
   sa.L = pb->num_layers;
   sa.S = pb->num_seqs;
   sa.W = pb->window;
@@ -229,7 +236,7 @@ int run_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void*
   sa.total_chunks = plan.total_chunks;
   const double scale = prm->scale > 0.0f ? (double)prm->scale : 1.0 / std::sqrt((double)d);
   sa.c = (float)(scale * 1.4426950408889634);  // log2(e)
-  return hip_status(launch_saliency(sa, d, st));
+  return hip_status(launch_saliency(sa, d, mode, st));
 }
 
 int run_priority(const stepkv_problem* pb, const stepkv_params* prm, const float* sal,
@@ -317,6 +324,57 @@ int stepkv_score(const stepkv_problem* pb, const stepkv_params* prm, const void*
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   float* sal = saliency ? saliency : reinterpret_cast<float*>(ws + w.sal);
   rc = run_saliency(pb, prm, q_win, k, sal, ws, st);
+  if (rc != STEPKV_OK) return rc;
+  return run_priority(pb, prm, sal, step_ids, protected_mask, step_utility, scores, step_stats,
+                      st);
+}
+
+int stepkv_window_lse(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                      const void* k, float* lse_win, void* workspace, size_t ws_bytes,
+                      void* stream) {
+  int rc = check_problem(pb);
+  if (rc == STEPKV_OK) rc = check_params(pb, prm);
+  if (rc != STEPKV_OK) return rc;
+  if (!q_win || !k || !lse_win) return STEPKV_EINVAL;
+  const WsLayout w = layout(pb, plan_saliency(pb));
+  if (!workspace || ws_bytes < w.sal || !aligned(workspace)) return STEPKV_EWORKSPACE;
+  // runs even without keys: every row then sees none and gets -inf
+  return run_saliency(pb, prm, q_win, k, nullptr, static_cast<uint8_t*>(workspace),
+                      static_cast<hipStream_t>(stream), SaliencyMode::kLseOnly, nullptr, lse_win);
+}
+
+int stepkv_saliency_from_lse(const stepkv_problem* pb, const stepkv_params* prm,
+                             const void* q_win, const void* k, const float* lse_win,
+                             float* saliency, void* workspace, size_t ws_bytes, void* stream) {
+  int rc = check_problem(pb);
+  if (rc == STEPKV_OK) rc = check_params(pb, prm);
+  if (rc != STEPKV_OK) return rc;
+  if (!q_win || !k || !lse_win || !saliency) return STEPKV_EINVAL;
+  const WsLayout w = layout(pb, plan_saliency(pb));
+  if (!workspace || ws_bytes < w.sal || !aligned(workspace)) return STEPKV_EWORKSPACE;
+  if (pb->cu_seqlens_host[pb->num_seqs] == 0) return STEPKV_OK;
+  return run_saliency(pb, prm, q_win, k, saliency, static_cast<uint8_t*>(workspace),
+                      static_cast<hipStream_t>(stream), SaliencyMode::kFromLse, lse_win);
+}
+
+int stepkv_score_from_lse(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                          const void* k, const float* lse_win, const int32_t* step_ids,
+                          const uint8_t* protected_mask, const float* step_utility,
+                          float* scores, float* saliency, stepkv_step_stat* step_stats,
+                          void* workspace, size_t ws_bytes, void* stream) {
+  int rc = check_problem(pb);
+  if (rc == STEPKV_OK) rc = check_params(pb, prm);
+  if (rc != STEPKV_OK) return rc;
+  if (!q_win || !k || !lse_win) return STEPKV_EINVAL;
+  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats);
+  if (rc != STEPKV_OK) return rc;
+  const WsLayout w = layout(pb, plan_saliency(pb));
+  if (!workspace || ws_bytes < w.total || !aligned(workspace)) return STEPKV_EWORKSPACE;
+  if (pb->cu_seqlens_host[pb->num_seqs] == 0) return STEPKV_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  float* sal = saliency ? saliency : reinterpret_cast<float*>(ws + w.sal);
+  rc = run_saliency(pb, prm, q_win, k, sal, ws, st, SaliencyMode::kFromLse, lse_win);
   if (rc != STEPKV_OK) return rc;
   return run_priority(pb, prm, sal, step_ids, protected_mask, step_utility, scores, step_stats,
                       st);

@@ -18,16 +18,22 @@ struct SaliencyArgs {
   float2* partial;           // [L*Hkv][total_chunks][rows_pad] (log2 max, sum)
   float* lse2;               // [S][L*Hkv][rows_pad] log2-domain log-sum-exp
   float* sal;                // [L*Hkv][Ntot] A_i
+  const float* lse_in;       // [L][S][W][Hq] natural-log row LSE given by the caller
+  float* lse_out;            // [L][S][W][Hq] natural-log row LSE exported (or null)
   int L, S, W, Hq, Hkv, G, R, rows_pad;
   int ntot, chunk, total_chunks;
-  float c;  // softmax scale * log2(e)
+  int causal;  // nonzero: window slot w sees keys 0 .. N_s - W + w only
+  float c;     // softmax scale * log2(e)
 };
 
 // Rows padded to whole row groups: 64, 128 or 256.
 int saliency_rows_pad(int R);
 // Key tile processed per iteration by one workgroup.
 int saliency_tile_keys(int R);
-hipError_t launch_saliency(const SaliencyArgs& a, int d, hipStream_t st);
+// Which sweeps to run: both (A from Q and K alone), the first one only (row
+// LSE, exported to lse_out), or the second one only (from lse_in).
+enum class SaliencyMode { kBoth, kLseOnly, kFromLse };
+hipError_t launch_saliency(const SaliencyArgs& a, int d, SaliencyMode mode, hipStream_t st);
 
 // ---------------------------------------------------------------- fuse
 struct FuseArgs {

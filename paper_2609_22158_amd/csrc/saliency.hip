@@ -210,7 +210,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
 #pragma unroll
   for (int st = 0; st < KSTEPS; ++st) fa[st] = kbuf_lds + tile_offset<D>(kr, (D / 16) * hf + st);
 
-  auto issue_tile = [&](int t, auto slot_c) {
+  auto issue_tile = [&](int t, auto slot_c) __attribute__((always_inline)) {
     constexpr int slot = decltype(slot_c)::value;
     const int kt = key0 + t * TILE;  // first key of the tile
     uint8_t* base = kbuf + slot * TILE_BYTES;
@@ -234,7 +234,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
       }
     }
   };
-  auto read_frags = [&](auto slot_c, bf16x8_t(&kf)[KSTEPS]) {
+  auto read_frags = [&](auto slot_c, bf16x8_t(&kf)[KSTEPS]) __attribute__((always_inline)) {
     constexpr int slot = decltype(slot_c)::value;
 #pragma unroll
     for (int st = 0; st < KSTEPS; ++st) kf[st] = lds_read_b128<slot * TILE_BYTES>(fa[st]);
@@ -266,7 +266,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     }
   }
 
-  auto reduce_tile = [&](int t) {  // pass 2: sum the per-wave column partials of tile t
+  auto reduce_tile = [&](int t) __attribute__((always_inline)) {  // pass 2: sum the per-wave column partials of tile t
     if (tid < TILE) {
       const int kg2 = tid >> 5, col2 = tid & 31;
       const float* rp = red + (t & 1) * kThreads;
@@ -282,7 +282,33 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     }
   };
 
-  auto mfma_tile = [&](const bf16x8_t(&kf)[KSTEPS], f32x16_t(&acc)[2]) {
+  // Causal tail: key i of the sequence is visible to window slot w only when
+  // i <= N_s - W + w. Only tiles reaching past N_s - W have hidden entries;
+  // their logits become -inf, which every later step maps to probability 0.
+  const int hidden_from = ns - a.W + 1;  // first key hidden from some window slot
+  auto tile_has_hidden = [&](int t) __attribute__((always_inline)) { return a.causal && key0 + (t + 1) * TILE > hidden_from; };
+  auto mask_hidden = [&](f32x16_t(&acc)[2], int t) __attribute__((always_inline)) {
+    // key kin of the tile is visible to window row `row` iff kin <= lim + row / G
+    const int lim = ns - a.W - key0 - t * TILE;
+    if (PASS == 1) {  // lane: one row per block; keys kg*32 + 4*hf + 8*(j/4) + (j%4)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int thr = lim + (rg * 64 + b * 32 + col) / a.G - kg * 32 - 4 * hf;
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if (8 * (j >> 2) + (j & 3) > thr) acc[b][j] = -INFINITY;
+      }
+    } else {  // lane: key kg*32 + col; rows rg*64 + 4*hf + 32*b + 8*(j/4) + (j%4)
+      // row / G >= kin - lim  <=>  row >= G * (kin - lim)
+      const int thr = a.G * (kg * 32 + col - lim) - rg * 64 - 4 * hf;
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if (b * 32 + 8 * (j >> 2) + (j & 3) < thr) acc[b][j] = -INFINITY;
+    }
+  };
+  auto mfma_tile = [&](const bf16x8_t(&kf)[KSTEPS], f32x16_t(&acc)[2]) __attribute__((always_inline)) {
     acc[0] = f32x16_t{};
     acc[1] = f32x16_t{};
 #pragma unroll
@@ -297,7 +323,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     }
   };
   // Softmax work on the last tile t, which may be partial (exact maxima).
-  auto finish_tile = [&](const f32x16_t(&acc)[2], int t, bool full) {
+  auto finish_tile = [&](const f32x16_t(&acc)[2], int t, bool full) __attribute__((always_inline)) {
     if (PASS == 1) {
       // lane: window row `col` of block b; keys t*TILE + kg*32 + 8*(j/4) + 4*hf + (j%4)
       const int kbase = t * TILE + kg * 32 + 4 * hf;
@@ -340,7 +366,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   // k-step waits only for its own K fragment. In pass 2 one wave per tile
   // (rotating) sums the column partials of tile t-1: its LDS reads are issued
   // first and consumed last.
-  auto body = [&](auto ic, int t, f32x16_t(&cur)[2], f32x16_t(&nxt)[2]) {
+  auto body = [&](auto ic, int t, f32x16_t(&cur)[2], f32x16_t(&nxt)[2]) __attribute__((always_inline)) {
     constexpr int i = decltype(ic)::value;
     constexpr int PER = 32 / (2 * KSTEPS);  // elements of `cur` per MFMA
     static_assert(PER * 2 * KSTEPS == 32, "slices cover 32 elements");
@@ -361,11 +387,12 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     }
     bf16x8_t kf[KSTEPS];
     read_frags(std::integral_constant<int, (i + 1) % NBUF>{}, kf);
+    if (tile_has_hidden(t)) mask_hidden(cur, t);
     __builtin_amdgcn_sched_barrier(0);
     nxt[0] = f32x16_t{};
     nxt[1] = f32x16_t{};
     float p4[2][4];
-    static_for<0, 2 * KSTEPS>([&](auto i2c) {
+    static_for<0, 2 * KSTEPS>([&](auto i2c) __attribute__((always_inline)) {
       constexpr int i2 = decltype(i2c)::value;
       constexpr int st = i2 >> 1, b = i2 & 1;
       if constexpr (b == 0) lds_wait<KSTEPS - 1 - st>(kf[st]);
@@ -395,11 +422,13 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
 #pragma unroll
           for (int j = 1; j < 16; ++j) tmax = fmaxf(tmax, cur[b][j]);
           const float mnew = fmaxf(m2[b], tmax * a.c);
-          float q4[4] = {0.f, 0.f, 0.f, 0.f};
+          if (mnew != -INFINITY) {  // -inf: every key this lane has seen is hidden
+            float q4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int j = 0; j < 16; ++j) q4[j & 3] += fast_exp2(fmaf(cur[b][j], a.c, -mnew));
-          zs[b] = fmaf(zs[b], fast_exp2(m2[b] - mnew), (q4[0] + q4[1]) + (q4[2] + q4[3]));
-          m2[b] = mnew;
+            for (int j = 0; j < 16; ++j) q4[j & 3] += fast_exp2(fmaf(cur[b][j], a.c, -mnew));
+            zs[b] = fmaf(zs[b], fast_exp2(m2[b] - mnew), (q4[0] + q4[1]) + (q4[2] + q4[3]));
+            m2[b] = mnew;
+          }
         }
         settle(zs[b]);  // keeps this iteration's VALU work inside this iteration
       }
@@ -418,7 +447,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     }
   };
 
-  static_for<0, NBUF - 1>([&](auto ic) {
+  static_for<0, NBUF - 1>([&](auto ic) __attribute__((always_inline)) {
     if (decltype(ic)::value < ntiles) issue_tile(decltype(ic)::value, ic);
   });
   wait_tiles<NLD, NBUF - 2>(min(NBUF - 2, ntiles - 1));  // tile 0 has landed
@@ -432,6 +461,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     mfma_tile(kf, acc_a);
   }
   if (PASS == 1 && ntiles > 1) {  // tile 0 is full: its maxima are the first references
+    if (tile_has_hidden(0)) mask_hidden(acc_a, 0);
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       float tmax = acc_a[b][0];
@@ -442,7 +472,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   }
   int t = 0;
   for (; t + NBUF < ntiles; t += NBUF) {  // ping-pong accumulators, no register copies
-    static_for<0, NBUF>([&](auto ic) {
+    static_for<0, NBUF>([&](auto ic) __attribute__((always_inline)) {
       if constexpr (decltype(ic)::value % 2 == 0)
         body(ic, t + decltype(ic)::value, acc_a, acc_b);
       else
@@ -450,7 +480,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     });
   }
   const int rest = ntiles - 1 - t;  // 0 .. NBUF-1 full tiles before the last one
-  static_for<0, NBUF - 1>([&](auto ic) {
+  static_for<0, NBUF - 1>([&](auto ic) __attribute__((always_inline)) {
     if (decltype(ic)::value < rest) {
       if constexpr (decltype(ic)::value % 2 == 0)
         body(ic, t + decltype(ic)::value, acc_a, acc_b);
@@ -463,7 +493,9 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   // t = ntiles - 1: the last, possibly partial, tile
   lds_barrier();
   if (PASS == 2 && t > 0) reduce_tile(t - 1);
-  finish_tile(last, t, (t + 1) * TILE <= nkeys);
+  f32x16_t fin[2] = {last[0], last[1]};  // a copy: writing through `last` would demote both
+  if (tile_has_hidden(t)) mask_hidden(fin, t);
+  finish_tile(fin, t, (t + 1) * TILE <= nkeys);
 
   if (PASS == 2) {
     lds_barrier();
@@ -512,8 +544,10 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
 }
 
 // Merge the per-chunk (max, sum) partials of one (sequence, head) into the
-// log2-domain log-sum-exp of every window row; padding rows get +inf so
-// that pass 2 gives them probability zero.
+// log2-domain log-sum-exp of every window row. Padding rows and rows that see
+// no key get +inf, so that the second sweep gives them probability zero; the
+// natural-log value of every real row is exported when lse_out is set (-inf
+// for a row that sees no key).
 __global__ void lse_combine_kernel(SaliencyArgs a) {
   const int LH = a.L * a.Hkv;
   const int s = blockIdx.x / LH, lh = blockIdx.x - s * LH;
@@ -528,16 +562,46 @@ __global__ void lse_combine_kernel(SaliencyArgs a) {
       M = Mn;
     }
   }
-  a.lse2[((size_t)s * LH + lh) * a.rows_pad + row] = (row < a.R) ? M + log2f(Z) : INFINITY;
+  const bool seen = row < a.R && Z > 0.f;
+  const float l2 = seen ? M + log2f(Z) : INFINITY;
+  a.lse2[((size_t)s * LH + lh) * a.rows_pad + row] = l2;
+  if (a.lse_out && row < a.R) {
+    const int l = lh / a.Hkv, h = lh - l * a.Hkv;
+    const int w = row / a.G, g = row - w * a.G;
+    a.lse_out[(((size_t)l * a.S + s) * a.W + w) * a.Hq + h * a.G + g] =
+        seen ? l2 * 0.693147180559945309f : -INFINITY;
+  }
+}
+
+// The caller's natural-log row LSE (lse_in [L][S][W][Hq]) in the layout and
+// log2 domain of the second sweep; -inf (a row that sees no key) and padding
+// rows become +inf.
+__global__ void lse_import_kernel(SaliencyArgs a) {
+  const int LH = a.L * a.Hkv;
+  const int s = blockIdx.x / LH, lh = blockIdx.x - s * LH;
+  const int row = threadIdx.x;
+  float l2 = INFINITY;
+  if (row < a.R) {
+    const int l = lh / a.Hkv, h = lh - l * a.Hkv;
+    const int w = row / a.G, g = row - w * a.G;
+    const float x = a.lse_in[(((size_t)l * a.S + s) * a.W + w) * a.Hq + h * a.G + g];
+    if (x != -INFINITY) l2 = x * 1.44269504088896341f;
+  }
+  a.lse2[((size_t)s * LH + lh) * a.rows_pad + row] = l2;
 }
 
 template <int D, int RG>
-hipError_t launch_passes(const SaliencyArgs& a, hipStream_t st) {
+hipError_t launch_passes(const SaliencyArgs& a, SaliencyMode mode, hipStream_t st) {
   const int LH = a.L * a.Hkv;
   const unsigned grid = (unsigned)LH * (unsigned)a.total_chunks;
-  hipLaunchKernelGGL((saliency_kernel<D, RG, 1>), dim3(grid), dim3(kThreads), 0, st, a);
-  hipLaunchKernelGGL(lse_combine_kernel, dim3(a.S * LH), dim3(a.rows_pad), 0, st, a);
-  hipLaunchKernelGGL((saliency_kernel<D, RG, 2>), dim3(grid), dim3(kThreads), 0, st, a);
+  if (mode != SaliencyMode::kFromLse) {
+    hipLaunchKernelGGL((saliency_kernel<D, RG, 1>), dim3(grid), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL(lse_combine_kernel, dim3(a.S * LH), dim3(a.rows_pad), 0, st, a);
+  } else {
+    hipLaunchKernelGGL(lse_import_kernel, dim3(a.S * LH), dim3(a.rows_pad), 0, st, a);
+  }
+  if (mode != SaliencyMode::kLseOnly)
+    hipLaunchKernelGGL((saliency_kernel<D, RG, 2>), dim3(grid), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 
@@ -546,20 +610,25 @@ hipError_t launch_passes(const SaliencyArgs& a, hipStream_t st) {
 int saliency_rows_pad(int R) { return R <= 64 ? 64 : (R <= 128 ? 128 : 256); }
 int saliency_tile_keys(int R) { return 32 * (4 / (saliency_rows_pad(R) / 64)); }
 
-hipError_t launch_saliency(const SaliencyArgs& a, int d, hipStream_t st) {
+hipError_t launch_saliency(const SaliencyArgs& a, int d, SaliencyMode mode, hipStream_t st) {
   hipLaunchKernelGGL(chunk_plan_kernel, dim3(1), dim3(64), 0, st, a.cu_seqlens, a.cu_chunks, a.S,
                      a.chunk);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.total_chunks == 0) return e;
+  if (e != hipSuccess) return e;
+  if (a.total_chunks == 0) {  // no keys at all: every exported row LSE is -inf
+    if (mode == SaliencyMode::kLseOnly)
+      hipLaunchKernelGGL(lse_combine_kernel, dim3(a.S * a.L * a.Hkv), dim3(a.rows_pad), 0, st, a);
+    return hipGetLastError();
+  }
   const int rg = a.rows_pad / 64;
   if (d == 128) {
-    if (rg == 1) return launch_passes<128, 1>(a, st);
-    if (rg == 2) return launch_passes<128, 2>(a, st);
-    return launch_passes<128, 4>(a, st);
+    if (rg == 1) return launch_passes<128, 1>(a, mode, st);
+    if (rg == 2) return launch_passes<128, 2>(a, mode, st);
+    return launch_passes<128, 4>(a, mode, st);
   }
-  if (rg == 1) return launch_passes<64, 1>(a, st);
-  if (rg == 2) return launch_passes<64, 2>(a, st);
-  return launch_passes<64, 4>(a, st);
+  if (rg == 1) return launch_passes<64, 1>(a, mode, st);
+  if (rg == 2) return launch_passes<64, 2>(a, mode, st);
+  return launch_passes<64, 4>(a, mode, st);
 }
 
 }  // namespace stepkv

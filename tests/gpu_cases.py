@@ -66,6 +66,11 @@ class GpuRun:
         return self.B.score(self.pb, self.q, self.k, self.sid, self.prot, self.util, self.params,
                             **kw)
 
+    def lse_tensor(self, lse_host: np.ndarray):
+        import torch
+
+        return torch.from_numpy(np.ascontiguousarray(lse_host, dtype=np.float32)).cuda()
+
     def select(self, scores, **kw):
         return self.B.select(self.pb, scores, self.prot, self.sid, self.budget, **kw)
 
@@ -75,20 +80,41 @@ class GpuRun:
 
 def oracle_params(p) -> O.Params:
     return O.Params(alpha=p.alpha, beta=p.beta, pool_kernel=p.pool_kernel,
-                    scale=(p.scale if p.scale > 0 else None))
+                    scale=(p.scale if p.scale > 0 else None), causal_tail=bool(p.causal_tail))
 
 
-def run_oracle(w, budget, params, heads=None, want_saliency=True):
-    """Oracle results keyed by (s, l, h); `heads` restricts it to some (l, h) pairs."""
+def oracle_lse(w, causal: bool, scale=None) -> np.ndarray:
+    """Window rows' natural-log log-sum-exp [L][S][W][Hq] from the oracle (fp64)."""
+    L, S, W, Hq, d = w.q_win.shape
+    G = w.group
+    sc = scale if scale is not None else 1.0 / math.sqrt(d)
+    out = np.empty((L, S, W, Hq))
+    for s in range(S):
+        a, b = int(w.cu_seqlens[s]), int(w.cu_seqlens[s + 1])
+        for l in range(L):
+            qs = O.decode_bf16(w.q_win[l, s])
+            for h in range(w.num_kv_heads):
+                rows = O.window_rows(qs, h, G)
+                keys = O.decode_bf16(w.k[l, h, a:b])
+                vis = O.visible_keys(b - a, W, G, causal)
+                out[l, s, :, h * G:(h + 1) * G] = O.window_row_lse(rows, keys, sc, vis).reshape(W, G)
+    return out
+
+
+def run_oracle(w, budget, params, heads=None, want_saliency=True, lse_win=None):
+    """Oracle results keyed by (s, l, h); `heads` restricts it to some (l, h) pairs.
+
+    lse_win (natural log, [L][S][W][Hq]) takes the saliency from given row LSEs."""
     S = oracle_utilities(w)
     args = (w.q_win, w.k, None, w.cu_seqlens, w.step_ids, w.protected, w.cu_steps, S, budget,
             oracle_params(params))
     if heads is None:
-        res = O.compress(*args, want_saliency=want_saliency)
+        res = O.compress(*args, want_saliency=want_saliency, lse_win=lse_win)
     else:
         res = None
         for l, h in heads:
-            part = O.compress(*args, layers=[l], heads=[h], want_saliency=want_saliency)
+            part = O.compress(*args, layers=[l], heads=[h], want_saliency=want_saliency,
+                              lse_win=lse_win)
             if res is None:
                 res = part
             else:

@@ -31,7 +31,7 @@ def _declared_functions():
 
 def test_exports_every_declared_function(lib):
     names = _declared_functions()
-    assert len(names) == 12, names
+    assert len(names) == 15, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGNATURES)
@@ -42,6 +42,7 @@ def test_defaults_are_the_papers(lib):
     assert (round(p.alpha, 6), round(p.beta, 6)) == (0.2, 0.8)
     assert (round(p.lambda_red, 6), round(p.w_r, 6), round(p.w_c, 6)) == (0.3, 0.85, 0.15)
     assert (p.r_min, p.r_max, p.s_max, p.eta, p.pool_kernel) == (-1.0, 2.0, 8.0, 1.5, 7)
+    assert p.causal_tail == 0  # every window row sees the whole sequence unless asked
 
 
 def test_strerror(lib):
@@ -186,3 +187,26 @@ def test_select_compact_decode_reject(lib):
                                        0.0, FAKE, None) == B.EUNSUPPORTED
     assert lib.stepkv_decode_attention(ctypes.byref(pb), FAKE, FAKE, FAKE, FAKE, 8,
                                        float("inf"), FAKE, None) == B.EINVAL
+
+
+def test_lse_entry_points_reject(lib):
+    """Validation of the LSE-fed calls: null arguments and short workspaces launch nothing."""
+    pb = _problem()
+    prm = B.Params().c()
+    need = lib.stepkv_saliency_workspace_bytes(ctypes.byref(pb))
+    P, R = ctypes.byref(pb), ctypes.byref(prm)
+    assert lib.stepkv_window_lse(P, R, FAKE, FAKE, None, FAKE * 16, need, None) == B.EINVAL
+    assert lib.stepkv_window_lse(P, R, FAKE, FAKE, FAKE, FAKE * 16, need - 256, None) == B.EWORKSPACE
+    assert lib.stepkv_window_lse(P, None, FAKE, FAKE, FAKE, FAKE * 16, need, None) == B.EINVAL
+    assert lib.stepkv_saliency_from_lse(P, R, FAKE, FAKE, None, FAKE, FAKE * 16, need,
+                                        None) == B.EINVAL
+    assert lib.stepkv_saliency_from_lse(P, R, FAKE, FAKE, FAKE, FAKE, FAKE * 16 + 8, need,
+                                        None) == B.EWORKSPACE  # misaligned
+    full = lib.stepkv_score_workspace_bytes(ctypes.byref(pb))
+    args = [FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, FAKE * 16]
+    assert lib.stepkv_score_from_lse(P, R, *args, full - 256, None) == B.EWORKSPACE
+    args[2] = None  # lse
+    assert lib.stepkv_score_from_lse(P, R, *args, full, None) == B.EINVAL
+    bad = _problem(W=65)
+    assert lib.stepkv_saliency_from_lse(ctypes.byref(bad), R, FAKE, FAKE, FAKE, FAKE, FAKE * 16,
+                                        need, None) == B.EUNSUPPORTED
