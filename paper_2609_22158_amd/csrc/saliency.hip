@@ -58,8 +58,10 @@ __device__ __forceinline__ void wait_tiles(int ahead) {
   }
 }
 
+// K ring per workgroup: four 8 KiB tiles at W*G = 256 rows, four 16 KiB tiles
+// at 128 rows, two 32 KiB tiles at 64 rows; two workgroups per CU fit in LDS.
 #ifndef STEPKV_SAL_RING_BYTES
-#define STEPKV_SAL_RING_BYTES 32768
+#define STEPKV_SAL_RING_BYTES (TILE_BYTES <= 8192 ? 32768 : 65536)
 #endif
 
 // Make the compiler wait for the load that produced x here, once, instead of
@@ -142,7 +144,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   constexpr int TILE = 32 * KG;               // keys per workgroup iteration
   constexpr int KSTEPS = D / 16;              // MFMA k-steps
   constexpr int TILE_BYTES = TILE * 2 * D;
-  // ring slots: an even count, 2 to 8
+  // ring slots: an even count, 2 to 8, within STEPKV_SAL_RING_BYTES
   constexpr int NBUF_FIT = STEPKV_SAL_RING_BYTES / TILE_BYTES;
   constexpr int NBUF = NBUF_FIT >= 8 ? 8 : (NBUF_FIT >= 2 ? NBUF_FIT & ~1 : 2);
   constexpr int NLD = TILE_BYTES / (kThreads * 16);  // 16-byte loads per thread per tile
