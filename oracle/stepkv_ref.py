@@ -31,6 +31,11 @@ attention-based saliency, Sec. 5.2):
   (P descending, position ascending); NaN ranks as -inf and -0.0 as +0.0;
   protected tokens are always kept and not counted in B (eq. problem).
 * Retained order is ascending position over protected and kept tokens.
+* Shared-index mode (the paper's setting: token saliency from the last 3
+  layers, App. D hyper-parameter table; one global ranking of a sequence's
+  tokens, Sec. 5.2): A is summed over the last n layers and all their KV
+  heads, pooled, normalised and fused once per sequence, and the one
+  retained set indexes the cache of every layer and head.
 * Step utility follows Algorithm 1, phases 1 and 2, boundary by boundary;
   gain_1 = 1 and red_1 = 0 by definition (Sec. 5.1.1); log is natural.
 
@@ -69,6 +74,7 @@ __all__ = [
     "decode_attention",
     "score_head",
     "compress",
+    "compress_shared",
 ]
 
 
@@ -379,4 +385,57 @@ def compress(q_win: np.ndarray, k: np.ndarray, v: Optional[np.ndarray], cu_seqle
                 if v is not None and v.size:
                     out["k_hat"][key] = k[l, h, a:b][idx]
                     out["v_hat"][key] = v[l, h, a:b][idx]
+    return out
+
+
+def compress_shared(q_win: np.ndarray, k: np.ndarray, v: Optional[np.ndarray],
+                    cu_seqlens: np.ndarray, step_ids: np.ndarray, protected: np.ndarray,
+                    cu_steps: np.ndarray, S: np.ndarray, budget: int, p: Params = Params(),
+                    last_layers: int = 3, seqs: Optional[Sequence[int]] = None,
+                    lse_win: Optional[np.ndarray] = None, want_kv: bool = True) -> Dict:
+    """Shared-index mode: one ranking per sequence from the last `last_layers` layers.
+
+    For sequence s: A[i] = sum over layers l >= L - last_layers and KV heads h of
+    that head's window saliency; T, T_hat and P follow from A as in the per-head
+    mode; one retained set K_s; the compacted cache of every (l, h) is K[l][h][K_s]
+    and V[l][h][K_s]. Results are keyed by s; k_hat / v_hat are [L][Hkv][R_s][d].
+    """
+    L, nseq, W, Hq, d = q_win.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    n = min(max(int(last_layers), 1), L)
+    scale = p.scale if p.scale is not None else 1.0 / math.sqrt(d)
+    out: Dict = {"P": {}, "idx": {}, "T_hat": {}, "A": {}, "k_hat": {}, "v_hat": {},
+                 "kept": {}}
+    for s in (range(nseq) if seqs is None else seqs):
+        a, b = int(cu_seqlens[s]), int(cu_seqlens[s + 1])
+        sid = step_ids[a:b]
+        prun = protected[a:b] == 0
+        Ss = np.asarray(S[int(cu_steps[s]):int(cu_steps[s + 1])], dtype=np.float64)
+        visible = visible_keys(b - a, W, G, True) if p.causal_tail else None
+        A = np.zeros(b - a)
+        for l in range(L - n, L):
+            qs = decode_bf16(q_win[l, s])
+            for h in range(Hkv):
+                rows = window_rows(qs, h, G)
+                keys = decode_bf16(k[l, h, a:b])
+                if lse_win is None:
+                    A = A + window_saliency(rows, keys, scale, visible)
+                else:
+                    lse = np.asarray(lse_win[l, s][:, h * G:(h + 1) * G],
+                                     dtype=np.float64).reshape(W * G)
+                    A = A + window_saliency_from_lse(rows, keys, scale, lse, visible)
+        T = pooled_saliency(A, prun, p.pool_kernel)
+        T_hat = normalised_saliency(T, prun)
+        P = priority(T_hat, sid, Ss, prun, p.alpha, p.beta)
+        idx = select_retained(P, prun, budget)
+        out["A"][s] = A
+        out["T_hat"][s] = T_hat
+        out["P"][s] = P
+        out["idx"][s] = idx
+        out["kept"][s] = kept_per_step(idx, sid, prun, Ss.shape[0])
+        if want_kv:
+            out["k_hat"][s] = k[:, :, a:b][:, :, idx]
+            if v is not None and v.size:
+                out["v_hat"][s] = v[:, :, a:b][:, :, idx]
     return out

@@ -399,3 +399,66 @@ def test_decode_attention_matches_torch_sdpa():
     np.testing.assert_allclose(O.decode_attention(q, K, V, 1 / 8), ref, rtol=1e-12)
     # one retained row: the output is that value row
     np.testing.assert_allclose(O.decode_attention(q, K[:1], V[:1], 1 / 8), V[0], rtol=1e-15)
+
+
+# ------------------------------------------------------------- shared-index mode
+def _shared_case(L=3, Hkv=2, G=2, W=4, d=64, n=60, n_steps=5, seed=12):
+    rng = np.random.default_rng(seed)
+    q = bits(rng.standard_normal((L, 1, W, Hkv * G, d)))
+    k = bits(rng.standard_normal((L, Hkv, n, d)) / math.sqrt(d))
+    v = bits(rng.standard_normal((L, Hkv, n, d)))
+    prot = np.zeros(n, np.uint8)
+    prot[:6] = 1
+    sid = np.concatenate([np.full(6, -1), np.sort(rng.integers(0, n_steps, n - 6))]).astype(np.int32)
+    S = rng.uniform(0.0, 1.7, n_steps)
+    return q, k, v, np.array([0, n]), sid, prot, np.array([0, n_steps]), S
+
+
+def test_shared_mode_single_head_is_the_per_head_mode():
+    """One layer, one KV head: the shared ranking is the per-head ranking."""
+    q, k, v, cu, sid, prot, cs, S = _shared_case(L=1, Hkv=1)
+    sh = O.compress_shared(q, k, v, cu, sid, prot, cs, S, 20, last_layers=3)
+    ph = O.compress(q, k, v, cu, sid, prot, cs, S, 20, want_saliency=True)
+    np.testing.assert_array_equal(sh["idx"][0], ph["idx"][(0, 0, 0)])
+    np.testing.assert_allclose(sh["P"][0], ph["P"][(0, 0, 0)], rtol=1e-15)
+
+
+def test_shared_mode_sums_only_the_last_layers():
+    """A sums to (layers used) x Hkv x W x G; layers before the last n have no influence."""
+    q, k, v, cu, sid, prot, cs, S = _shared_case(L=4)
+    sh = O.compress_shared(q, k, v, cu, sid, prot, cs, S, 20, last_layers=3)
+    assert abs(sh["A"][0].sum() - 3 * 2 * 4 * 2) < 1e-10
+    q2, k2 = q.copy(), k.copy()
+    q2[0] = bits(np.random.default_rng(99).standard_normal(q2[0].shape))  # layer 0 is not used
+    k2[0] = bits(np.random.default_rng(98).standard_normal(k2[0].shape))
+    sh2 = O.compress_shared(q2, k2, v, cu, sid, prot, cs, S, 20, last_layers=3)
+    np.testing.assert_array_equal(sh2["A"][0], sh["A"][0])
+    np.testing.assert_array_equal(sh2["idx"][0], sh["idx"][0])
+    one = O.compress_shared(q, k, v, cu, sid, prot, cs, S, 20, last_layers=1)
+    assert abs(one["A"][0].sum() - 2 * 4 * 2) < 1e-10
+
+
+def test_shared_mode_pooling_is_linear_over_heads():
+    """T_hat of the summed A equals the normalised sum of the per-head pooled T (pooling is linear)."""
+    q, k, v, cu, sid, prot, cs, S = _shared_case(L=3)
+    sh = O.compress_shared(q, k, v, cu, sid, prot, cs, S, 20, last_layers=3)
+    ph = O.compress(q, k, v, cu, sid, prot, cs, S, 20, want_saliency=True)
+    prun = prot == 0
+    T = sum(O.pooled_saliency(ph["A"][(0, l, h)], prun, 7) for l in range(3) for h in range(2))
+    np.testing.assert_allclose(sh["T_hat"][0], T / T[prun].max(), rtol=1e-12)
+
+
+def test_shared_mode_one_index_set_for_every_head():
+    """k_hat / v_hat of every (layer, head) gather the same positions, in order."""
+    q, k, v, cu, sid, prot, cs, S = _shared_case(L=3, n=80)
+    sh = O.compress_shared(q, k, v, cu, sid, prot, cs, S, 25, last_layers=2)
+    idx = sh["idx"][0]
+    assert len(idx) == 6 + 25 and (np.diff(idx) > 0).all() and set(range(6)) <= set(idx.tolist())
+    for l in range(3):
+        for h in range(2):
+            np.testing.assert_array_equal(sh["k_hat"][0][l, h], k[l, h][idx])
+            np.testing.assert_array_equal(sh["v_hat"][0][l, h], v[l, h][idx])
+    # the shared ranking is the top of P by (P desc, position asc), as Python's sorted() orders it
+    P = sh["P"][0]
+    order = sorted((i for i in range(80) if prot[i] == 0), key=lambda i: (-P[i], i))[:25]
+    assert sorted(order) == [int(i) for i in idx if prot[i] == 0]
