@@ -1,10 +1,11 @@
 #!/usr/bin/env python3
 """Throughput of the StepKV compression pass on one MI355X.
 
-One step = the whole pass over one synthetic batch: host step-utility update
-(Algorithm 1 phases 1-2) -> saliency -> priority -> top-B select -> K/V
-compaction, all layers and KV heads. Inputs are resident in HBM before the
-timed region. Prints one JSON line.
+One step = the whole pass over one synthetic batch at one pruning boundary:
+host step-utility update for the newest step of every sequence (Algorithm 1
+phases 1-2, from the state of the boundaries before it) -> saliency ->
+priority -> top-B select -> K/V compaction, all layers and KV heads. Inputs
+are resident in HBM before the timed region. Prints one JSON line.
 
 By default the saliency is computed from the window queries and the cache
 alone (two sweeps over K). With --lse-fed the window rows' log-sum-exps are
@@ -50,6 +51,9 @@ def parse():
                     help="take the window rows' log-sum-exps as an input (one sweep over K)")
     ap.add_argument("--causal-tail", action="store_true",
                     help="window slot w sees keys up to N - W + w only (causal prefill)")
+    ap.add_argument("--shared-layers", type=int, default=0,
+                    help="shared-index mode: rank each sequence once from the saliency of its "
+                         "last N layers and compact every layer and head with that one set")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this size (HBM counter calibration)")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -205,6 +209,35 @@ def cpu_baseline(w, budget, seconds, params, lse_fed=False):
                       f"x {w.num_kv_heads} KV heads"}
 
 
+def cpu_baseline_shared(w, budget, seconds, params, last_layers):
+    """Time the oracle's shared-index pass, one sequence at a time, until `seconds` pass."""
+    import oracle as O
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    S = np.concatenate([O.run_step_updates(g.valid, g.gain, g.red, g.obs_sim.astype(np.float64),
+                                           O.Params())[2] for g in w.signals])
+    op = O.Params(causal_tail=bool(params.causal_tail))
+    done, tokens, dt = 0, 0, 0.0
+    for s in range(w.num_seqs):
+        t0 = time.perf_counter()
+        O.compress_shared(w.q_win, w.k, w.v, w.cu_seqlens, w.step_ids, w.protected, w.cu_steps,
+                          S, budget, op, last_layers=last_layers, seqs=[s])
+        dt += time.perf_counter() - t0
+        done += 1
+        tokens += w.seqlens[s]
+        if dt >= seconds:
+            break
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} of {w.num_seqs} sequence(s) ({tokens} tokens), shared-index pass "
+                      f"over the last {last_layers} layers and all {w.num_layers} layers' "
+                      f"compaction, in {dt:.1f} s"}
+
+
 def main():
     args = parse()
     if args.record_traffic:
@@ -258,12 +291,28 @@ def main():
         lse = B.window_lse(pb, q, k, params, workspace=ws)
         torch.cuda.synchronize()
 
-    def step(ev=None):
-        # a0: host step utility (Algorithm 1 phases 1-2) for every sequence
-        S = np.concatenate([B.step_utilities(g.valid, g.gain, g.red, g.obs_sim)
-                            for g in w.signals])
-        util_pinned.numpy()[:] = S
+    # a0 state: every trajectory's step utilities up to the boundary before its last step
+    trackers, snaps = [], []
+    for g in w.signals:
+        tr = B.StepTracker(g.num_steps)
+        for t in range(g.num_steps - 1):
+            tr.update(g.valid[t], g.gain[t], g.red[t], g.obs_sim[t, :t])
+        trackers.append(tr)
+        snaps.append(tr.snapshot())
+    util_host = util_pinned.numpy()
+    cu_steps = [int(x) for x in w.cu_steps]
+
+    def host_update():
+        # a0: the boundary after each sequence's newest step (Algorithm 1 phases 1-2)
+        for i, (g, tr) in enumerate(zip(w.signals, trackers)):
+            tr.restore(snaps[i])  # every timed step redoes the same boundary
+            t = g.num_steps - 1
+            tr.update(g.valid[t], g.gain[t], g.red[t], g.obs_sim[t, :t],
+                      out=util_host[cu_steps[i]:cu_steps[i + 1]])
         util.copy_(util_pinned, non_blocking=True)
+
+    def step(ev=None):
+        host_update()
         if ev:
             ev[0].record(stream)
         if lse is None:
@@ -282,6 +331,29 @@ def main():
         if ev:
             ev[4].record(stream)
 
+    shared = args.shared_layers > 0
+    if shared:
+        n_sh = min(args.shared_layers, L)
+        scores_sh = torch.empty(ntot, dtype=torch.float32, device=dev)
+        idx_sh = torch.empty(ntot, dtype=torch.int32, device=dev)
+        ws_sh = torch.empty(max(int(B.load().stepkv_score_shared_workspace_bytes(
+            B.ctypes.byref(pb.c), n_sh)), 1), dtype=torch.uint8, device=dev)
+
+        def step(ev=None):  # noqa: F811 - the shared-index pass
+            host_update()
+            if ev:
+                ev[0].record(stream)
+            B.score_shared(pb, q, k, sid, prot, util, params, last_layers=n_sh, lse=lse,
+                           workspace=ws_sh, scores=scores_sh)
+            if ev:
+                ev[1].record(stream)
+            B.select_shared(pb, scores_sh, prot, sid, budget, idx=idx_sh, cu_retained=cu_ret)
+            if ev:
+                ev[2].record(stream)
+            B.compact_shared(pb, k, v, idx_sh, cu_ret, out_rows, k_out=k_out, v_out=v_out)
+            if ev:
+                ev[3].record(stream)
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -294,7 +366,10 @@ def main():
         torch.cuda.synchronize()
         del src_buf, dst_buf
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    stage_names = (["score", "select", "compact"] if shared
+                   else ["saliency", "priority", "select", "compact"])
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stage_names) + 1)]
+           for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -307,7 +382,6 @@ def main():
     wall = time.perf_counter() - wall0
     total_ms = t_start.elapsed_time(t_end)
     ms_per_step = max(total_ms, wall * 1e3) / args.steps
-    stage_names = ["saliency", "priority", "select", "compact"]
     stage_ms = {n: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
                 for i, n in enumerate(stage_names)}
 
@@ -316,20 +390,24 @@ def main():
     G = w.num_q_heads // Hkv
     R = w.window * G
     lh = L * Hkv
-    # algorithmic work per launch of the saliency stage
+    # algorithmic work per launch of the saliency stage (in shared mode: the
+    # scoring call, whose sweeps cover the last n layers only)
     sweeps = 1 if args.lse_fed else 2
-    k_bytes = lh * ntot * d * 2
-    sal_flops = sweeps * 2 * R * d * ntot * lh         # Q K^T once per sweep
-    sal_bytes = k_bytes + lh * ntot * 4 + q.numel() * 2  # K once, A written, Q read
+    lh_sal = (n_sh * Hkv) if shared else lh
+    k_bytes = lh_sal * ntot * d * 2
+    sal_flops = sweeps * 2 * R * d * ntot * lh_sal     # Q K^T once per sweep
+    sal_bytes = k_bytes + lh_sal * ntot * 4 + q.numel() * 2 * lh_sal // lh  # K, A, Q
     if args.lse_fed:
-        sal_bytes += lse.numel() * 4
+        sal_bytes += lse.numel() * 4 * lh_sal // lh
     compact_bytes = lh * out_rows * d * 2 * 2 * 2     # K and V rows, read and written
-    t_sal = stage_ms["saliency"] * 1e-3
+    t_sal = stage_ms["score" if shared else "saliency"] * 1e-3
     t_cmp = stage_ms["compact"] * 1e-3
     achieved_tflops = sal_flops / t_sal / 1e12
     achieved_gbs = sal_bytes / t_sal / 1e9
     kernel = ("saliency (one MFMA sweep over K, row LSE given)" if args.lse_fed
               else "saliency (two MFMA sweeps over K)")
+    if shared:
+        kernel = f"shared-index scoring: {kernel} of the last {n_sh} layers, head sum, priority"
     traffic = recorded_traffic(traffic_key(args.workload, budget, w.window, args.lse_fed))
     # the binding roofline: whichever of HBM and MFMA needs longer at peak
     if sal_bytes / (HBM_PEAK_GBS * 1e9) >= sal_flops / (BF16_PEAK_TFLOPS * 1e12):
@@ -356,7 +434,10 @@ def main():
                                f"{'...' if w.num_seqs > 4 else ''} tokens, window {w.window}, "
                                f"budget {budget} per KV head"
                                + (", row LSE given" if args.lse_fed else "")
-                               + (", causal window" if args.causal_tail else ""),
+                               + (", causal window" if args.causal_tail else "")
+                               + (f", one ranking per sequence from the last {n_sh} layers"
+                                  if shared else ""),
+                   "shared_layers": n_sh if shared else 0,
                    "saliency_sweeps": sweeps, "causal_tail": bool(args.causal_tail),
                    "layers": L, "kv_heads": Hkv, "q_heads": w.num_q_heads, "head_dim": d,
                    "seq_len": int(max(w.seqlens)), "tokens": int(ntot), "window": w.window,
@@ -367,7 +448,9 @@ def main():
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, budget, args.cpu_seconds, params, args.lse_fed)
+        line["cpu_baseline"] = (cpu_baseline_shared(w, budget, args.cpu_seconds, params, n_sh)
+                                if shared else
+                                cpu_baseline(w, budget, args.cpu_seconds, params, args.lse_fed))
     print(json.dumps(line), flush=True)
 
 

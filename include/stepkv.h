@@ -18,6 +18,9 @@
  *   stepkv_select   global top-B ranking per (sequence, layer, KV head)
  *                   (Sec. 5.2 last paragraph; Algorithm 1 phase 3)
  *   stepkv_compact  C_hat = C_prot || C_traj[K] (eq. problem)
+ *   stepkv_*_shared the same three steps with one ranking per sequence from
+ *                   the last layers' saliency and one retained set for every
+ *                   layer and head (App. D; Sec. 5.2)
  *
  * Host-only helpers implement the budget rule B_t = max(1, floor(rho N_t))
  * (eq. problem) and the step-utility update of Algorithm 1 phases 1-2
@@ -243,6 +246,50 @@ int stepkv_score_from_lse(const stepkv_problem* pb, const stepkv_params* prm, co
                           const uint8_t* protected_mask, const float* step_utility,
                           float* scores, float* saliency, stepkv_step_stat* step_stats,
                           void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------- shared-index mode
+ * The paper's own setting: token saliency from the last 3 layers (App. D,
+ * hyper-parameter table) and one global ranking of each sequence's tokens
+ * (Sec. 5.2), so that a single retained set indexes the cache of every layer
+ * and KV head. Sequence-level outputs have one row per sequence:
+ *   scores, saliency fp32 [Ntot]; idx int32 [Ntot]; step_stats and
+ *   kept_per_step [cu_steps[S]].
+ */
+
+/* Bytes of device workspace stepkv_score_shared needs (0 when invalid). */
+size_t stepkv_score_shared_workspace_bytes(const stepkv_problem* pb, int32_t last_layers);
+
+/* Shared-index scoring. With n = min(last_layers, L) and layers L-n .. L-1:
+ *   A_i  = sum over those layers l and KV heads h of A_i(l, h)
+ *          (stepkv_saliency's A; from lse_win as in stepkv_saliency_from_lse
+ *          when lse_win, fp32 [L][S][W][Hq], is non-NULL)
+ *   T_i, Th_i, P_i as in stepkv_score, once per sequence.
+ * scores (required) and saliency (= the summed A, optional) are fp32 [Ntot];
+ * step_stats is [cu_steps[S]] (optional). Errors as stepkv_score, plus EINVAL
+ * for last_layers < 1; EWORKSPACE below stepkv_score_shared_workspace_bytes. */
+int stepkv_score_shared(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                        const void* k, const float* lse_win, int32_t last_layers,
+                        const int32_t* step_ids, const uint8_t* protected_mask,
+                        const float* step_utility, float* scores, float* saliency,
+                        stepkv_step_stat* step_stats, void* workspace, size_t ws_bytes,
+                        void* stream);
+
+/* Shared-index selection: stepkv_select over one score row per sequence
+ * (scores fp32 [Ntot]); writes idx int32 [Ntot] (ascending local positions of
+ * sequence s at offset cu_seqlens[s]), cu_retained [S+1] and optionally
+ * kept_per_step [cu_steps[S]]. Budgets as stepkv_select (e.g. B_t from
+ * stepkv_budget_from_ratio per sequence via `budgets`). Errors as stepkv_select. */
+int stepkv_select_shared(const stepkv_problem* pb, const float* scores,
+                         const uint8_t* protected_mask, const int32_t* step_ids, int32_t budget,
+                         const int32_t* budgets, int32_t* idx, int32_t* cu_retained,
+                         int32_t* kept_per_step, void* stream);
+
+/* Shared-index compaction (eq. problem with one retained set per sequence):
+ * every (layer, KV head) row of k_out / v_out [L][Hkv][out_rows][d] gathers
+ * the positions idx int32 [Ntot] of its own cache. Errors as stepkv_compact. */
+int stepkv_compact_shared(const stepkv_problem* pb, const void* k, const void* v,
+                          const int32_t* idx, const int32_t* cu_retained, int32_t out_rows,
+                          void* k_out, void* v_out, void* stream);
 
 /* Sec. 5.2 / Algorithm 1 phase 3 / eq. problem: for every (sequence, layer,
  * KV head), keep every protected token plus exactly min(B, N_pr) prunable

@@ -10,8 +10,10 @@ from .binding import (  # noqa: F401
     Params,
     Problem,
     StepKVError,
+    StepTracker,
     budget_from_ratio,
     compact,
+    compact_shared,
     compress,
     decode_attention,
     decode_stats,
@@ -21,7 +23,9 @@ from .binding import (  # noqa: F401
     saliency,
     saliency_from_lse,
     score,
+    score_shared,
     select,
+    select_shared,
     step_utilities,
     window_lse,
 )

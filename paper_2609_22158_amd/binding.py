@@ -97,6 +97,15 @@ _SIGNATURES = {
     "stepkv_score_from_lse": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC),
                                              _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                              ctypes.c_size_t, _vp]),
+    "stepkv_score_shared_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC),
+                                                            ctypes.c_int32]),
+    "stepkv_score_shared": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp,
+                                           _vp, _vp, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp,
+                                           _vp, _vp, ctypes.c_size_t, _vp]),
+    "stepkv_select_shared": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, _vp, _vp,
+                                            ctypes.c_int32, _vp, _vp, _vp, _vp, _vp]),
+    "stepkv_compact_shared": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, _vp, _vp, _vp,
+                                             ctypes.c_int32, _vp, _vp, _vp]),
     "stepkv_select": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, _vp, _vp, ctypes.c_int32,
                                      _vp, _vp, _vp, _vp, _vp]),
     "stepkv_compact": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, _vp, _vp, _vp,
@@ -196,6 +205,53 @@ def step_utilities(valid: Sequence[float], gain: Sequence[float], red: Sequence[
                                     ctypes.byref(p), S.ctypes.data_as(_f32p))
         _check("stepkv_step_update", rc)
     return S[:n].copy()
+
+
+class StepTracker:
+    """Step-utility state of one trajectory across pruning boundaries (Algorithm 1
+    phases 1-2, one stepkv_step_update per boundary). `update` adds step t and
+    returns (or writes into `out`) the utilities S_0..S_t as float32."""
+
+    def __init__(self, capacity: int, params: Optional[Params] = None):
+        self.capacity = max(int(capacity), 1)
+        self.r = np.zeros(self.capacity, np.float64)
+        self.c = np.zeros(self.capacity, np.float64)
+        self.S = np.zeros(self.capacity, np.float32)
+        self._p = (params or Params()).c()
+        self._st = StepStateC(self.capacity, 0, self.r.ctypes.data_as(_f64p),
+                              self.c.ctypes.data_as(_f64p))
+
+    @property
+    def num_steps(self) -> int:
+        return int(self._st.num_steps)
+
+    def update(self, valid: float, gain: float, red: float, sim_prev=None, out=None) -> np.ndarray:
+        """Boundary after step t = num_steps: sim_prev[k] = sim(Obs_t, Obs_k) for k < t."""
+        t = self.num_steps
+        row = None
+        if t > 0:
+            row = np.ascontiguousarray(sim_prev, dtype=np.float32)
+            if row.shape != (t,):
+                raise ValueError(f"sim_prev: shape {row.shape}, expected ({t},)")
+        dst = self.S if out is None else out
+        if out is not None and (out.dtype != np.float32 or not out.flags.c_contiguous
+                                or out.shape[0] < t + 1):
+            raise ValueError("out: a contiguous float32 array of at least t + 1 entries")
+        rc = load().stepkv_step_update(ctypes.byref(self._st), float(valid), float(gain),
+                                       float(red), row.ctypes.data_as(_f32p) if row is not None
+                                       else None, ctypes.byref(self._p),
+                                       dst.ctypes.data_as(_f32p))
+        _check("stepkv_step_update", rc)
+        return dst[:t + 1]
+
+    def snapshot(self):
+        return self.r.copy(), self.c.copy(), self.num_steps
+
+    def restore(self, snap) -> None:
+        r, c, n = snap
+        self.r[:] = r
+        self.c[:] = c
+        self._st.num_steps = n
 
 
 # ---------------------------------------------------------------- problem
@@ -396,6 +452,95 @@ def priority(pb: Problem, sal, step_ids, protected, step_utility,
     if stats is not None:
         out["stats_raw"] = stats
     return out
+
+
+def score_shared(pb: Problem, q_win, k, step_ids, protected, step_utility,
+                 params: Optional[Params] = None, *, last_layers: int = 3, lse=None,
+                 want_saliency: bool = False, want_stats: bool = False, workspace=None,
+                 scores=None, stream=None):
+    """stepkv_score_shared: one priority row per sequence, P [Ntot], from the saliency of
+    the last `last_layers` layers summed over their KV heads (optionally from row LSEs)."""
+    import torch
+
+    lib = load()
+    L, Hkv, d, W, S = pb.num_layers, pb.num_kv_heads, pb.head_dim, pb.window, pb.num_seqs
+    dev = pb.device
+    qp = _need(q_win, torch.bfloat16, (L, S, W, pb.num_q_heads, d), "q_win")
+    kp = _need(k, torch.bfloat16, (L, Hkv, pb.ntot, d), "k")
+    lp = _need(lse, torch.float32, (L, S, W, pb.num_q_heads), "lse") if lse is not None else None
+    sp = _need(step_ids, torch.int32, (pb.ntot,), "step_ids")
+    pp = _need(protected, torch.uint8, (pb.ntot,), "protected")
+    up = _need(step_utility, torch.float32, (pb.total_steps,), "step_utility")
+    if scores is None:
+        scores = torch.empty(pb.ntot, dtype=torch.float32, device=dev)
+    _need(scores, torch.float32, (pb.ntot,), "scores")
+    sal = torch.empty(pb.ntot, dtype=torch.float32, device=dev) if want_saliency else None
+    stats = (torch.empty((pb.total_steps, 2), dtype=torch.int64, device=dev)
+             if want_stats else None)
+    if workspace is None:
+        need = int(lib.stepkv_score_shared_workspace_bytes(ctypes.byref(pb.c), last_layers))
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lib.stepkv_score_shared(ctypes.byref(pb.c), ctypes.byref((params or Params()).c()), qp,
+                                 kp, lp, last_layers, sp, pp, up, scores.data_ptr(),
+                                 sal.data_ptr() if sal is not None else None,
+                                 stats.data_ptr() if stats is not None else None,
+                                 workspace.data_ptr(), workspace.numel(), _stream(stream))
+    _check("stepkv_score_shared", rc)
+    out = {"scores": scores}
+    if sal is not None:
+        out["saliency"] = sal
+    if stats is not None:
+        out["stats_raw"] = stats
+    return out
+
+
+def select_shared(pb: Problem, scores, protected, step_ids, budget: int, *, budgets=None,
+                  want_kept: bool = False, idx=None, cu_retained=None, stream=None):
+    """stepkv_select_shared: one retained set per sequence, idx [Ntot]."""
+    import torch
+
+    lib = load()
+    dev = pb.device
+    sp_ = _need(scores, torch.float32, (pb.ntot,), "scores")
+    pp = _need(protected, torch.uint8, (pb.ntot,), "protected")
+    ip = _need(step_ids, torch.int32, (pb.ntot,), "step_ids")
+    bp = _need(budgets, torch.int32, (pb.num_seqs,), "budgets") if budgets is not None else None
+    if idx is None:
+        idx = torch.empty(pb.ntot, dtype=torch.int32, device=dev)
+    if cu_retained is None:
+        cu_retained = torch.empty(pb.num_seqs + 1, dtype=torch.int32, device=dev)
+    kept = torch.empty(pb.total_steps, dtype=torch.int32, device=dev) if want_kept else None
+    rc = lib.stepkv_select_shared(ctypes.byref(pb.c), sp_, pp, ip, int(budget), bp,
+                                  idx.data_ptr(), cu_retained.data_ptr(),
+                                  kept.data_ptr() if kept is not None else None, _stream(stream))
+    _check("stepkv_select_shared", rc)
+    out = {"idx": idx, "cu_retained": cu_retained}
+    if kept is not None:
+        out["kept"] = kept
+    return out
+
+
+def compact_shared(pb: Problem, k, v, idx, cu_retained, out_rows: int, *, k_out=None, v_out=None,
+                   stream=None):
+    """stepkv_compact_shared: every (layer, KV head) gathers the same positions idx [Ntot]."""
+    import torch
+
+    lib = load()
+    L, Hkv, d = pb.num_layers, pb.num_kv_heads, pb.head_dim
+    kp = _need(k, torch.bfloat16, (L, Hkv, pb.ntot, d), "k")
+    vp = _need(v, torch.bfloat16, (L, Hkv, pb.ntot, d), "v")
+    ip = _need(idx, torch.int32, (pb.ntot,), "idx")
+    cp = _need(cu_retained, torch.int32, (pb.num_seqs + 1,), "cu_retained")
+    if k_out is None:
+        k_out = torch.empty((L, Hkv, out_rows, d), dtype=torch.bfloat16, device=pb.device)
+    if v_out is None:
+        v_out = torch.empty_like(k_out)
+    _need(k_out, torch.bfloat16, (L, Hkv, out_rows, d), "k_out")
+    _need(v_out, torch.bfloat16, (L, Hkv, out_rows, d), "v_out")
+    rc = lib.stepkv_compact_shared(ctypes.byref(pb.c), kp, vp, ip, cp, int(out_rows),
+                                   k_out.data_ptr(), v_out.data_ptr(), _stream(stream))
+    _check("stepkv_compact_shared", rc)
+    return k_out, v_out
 
 
 def decode_stats(stats_raw) -> dict:

@@ -274,6 +274,40 @@ int check_priority_args(const stepkv_problem* pb, const int32_t* step_ids,
 
 bool aligned(const void* p) { return reinterpret_cast<uintptr_t>(p) % kAlign == 0; }
 
+// Shared-index mode: the last n layers, as a problem of their own, plus the
+// one-"head" view of the per-sequence ranking (one score row per sequence).
+int shared_layers(const stepkv_problem* pb, int32_t last_layers) {
+  return std::min<int>(std::max<int>(last_layers, 1), pb->num_layers);
+}
+
+stepkv_problem last_layers_view(const stepkv_problem* pb, int n) {
+  stepkv_problem sub = *pb;
+  sub.num_layers = n;
+  return sub;
+}
+
+stepkv_problem one_head_view(const stepkv_problem* pb) {
+  stepkv_problem one = *pb;
+  one.num_layers = 1;
+  one.num_q_heads = 1;
+  one.num_kv_heads = 1;
+  return one;
+}
+
+struct SharedLayout {
+  size_t heads, shared, total;  // per-head saliency [n*Hkv][Ntot], summed A [Ntot]
+};
+
+SharedLayout shared_layout(const stepkv_problem* pb, int n) {
+  const stepkv_problem sub = last_layers_view(pb, n);
+  const size_t ntot = (size_t)pb->cu_seqlens_host[pb->num_seqs];
+  SharedLayout w;
+  w.heads = layout(&sub, plan_saliency(&sub)).sal;  // after the sweep workspace
+  w.shared = align_up(w.heads + sizeof(float) * n * pb->num_kv_heads * ntot);
+  w.total = align_up(w.shared + sizeof(float) * ntot);
+  return w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -380,6 +414,84 @@ int stepkv_score_from_lse(const stepkv_problem* pb, const stepkv_params* prm, co
                       st);
 }
 
+size_t stepkv_score_shared_workspace_bytes(const stepkv_problem* pb, int32_t last_layers) {
+  if (check_problem(pb) != STEPKV_OK || last_layers < 1) return 0;
+  return shared_layout(pb, shared_layers(pb, last_layers)).total;
+}
+
+int stepkv_score_shared(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                        const void* k, const float* lse_win, int32_t last_layers,
+                        const int32_t* step_ids, const uint8_t* protected_mask,
+                        const float* step_utility, float* scores, float* saliency,
+                        stepkv_step_stat* step_stats, void* workspace, size_t ws_bytes,
+                        void* stream) {
+  int rc = check_problem(pb);
+  if (rc == STEPKV_OK) rc = check_params(pb, prm);
+  if (rc != STEPKV_OK) return rc;
+  if (!q_win || !k || last_layers < 1) return STEPKV_EINVAL;
+  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats);
+  if (rc != STEPKV_OK) return rc;
+  const int n = shared_layers(pb, last_layers);
+  const SharedLayout w = shared_layout(pb, n);
+  if (!workspace || ws_bytes < w.total || !aligned(workspace)) return STEPKV_EWORKSPACE;
+  const int ntot = pb->cu_seqlens_host[pb->num_seqs];
+  if (ntot == 0) return STEPKV_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  // the last n layers of q_win, k and lse_win
+  const size_t first = (size_t)(pb->num_layers - n);
+  const size_t q_layer = (size_t)pb->num_seqs * pb->window * pb->num_q_heads;  // rows per layer
+  const uint16_t* q = static_cast<const uint16_t*>(q_win) + first * q_layer * pb->head_dim;
+  const uint16_t* kk =
+      static_cast<const uint16_t*>(k) + first * pb->num_kv_heads * (size_t)ntot * pb->head_dim;
+  const float* lse = lse_win ? lse_win + first * q_layer : nullptr;
+  const stepkv_problem sub = last_layers_view(pb, n);
+  float* heads = reinterpret_cast<float*>(ws + w.heads);
+  rc = run_saliency(&sub, prm, q, kk, heads, ws, st,
+                    lse ? SaliencyMode::kFromLse : SaliencyMode::kBoth, lse);
+  if (rc != STEPKV_OK) return rc;
+  float* sal = saliency ? saliency : reinterpret_cast<float*>(ws + w.shared);
+  rc = hip_status(launch_sum_heads(heads, n * pb->num_kv_heads, ntot, sal, st));
+  if (rc != STEPKV_OK) return rc;
+  const stepkv_problem one = one_head_view(pb);
+  return run_priority(&one, prm, sal, step_ids, protected_mask, step_utility, scores, step_stats,
+                      st);
+}
+
+int stepkv_select_shared(const stepkv_problem* pb, const float* scores,
+                         const uint8_t* protected_mask, const int32_t* step_ids, int32_t budget,
+                         const int32_t* budgets, int32_t* idx, int32_t* cu_retained,
+                         int32_t* kept_per_step, void* stream) {
+  const int rc = check_problem(pb);
+  if (rc != STEPKV_OK) return rc;
+  const stepkv_problem one = one_head_view(pb);
+  return stepkv_select(&one, scores, protected_mask, step_ids, budget, budgets, idx, cu_retained,
+                       kept_per_step, stream);
+}
+
+int stepkv_compact_shared(const stepkv_problem* pb, const void* k, const void* v,
+                          const int32_t* idx, const int32_t* cu_retained, int32_t out_rows,
+                          void* k_out, void* v_out, void* stream) {
+  const int rc = check_problem(pb);
+  if (rc != STEPKV_OK) return rc;
+  if (!k || !v || !idx || !cu_retained || !k_out || !v_out || out_rows < 0) return STEPKV_EINVAL;
+  CompactArgs a;
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.idx = idx;
+  a.cu_seqlens = pb->cu_seqlens;
+  a.cu_retained = cu_retained;
+  a.k_out = static_cast<uint16_t*>(k_out);
+  a.v_out = static_cast<uint16_t*>(v_out);
+  a.S = pb->num_seqs;
+  a.LH = pb->num_layers * pb->num_kv_heads;
+  a.ntot = pb->cu_seqlens_host[pb->num_seqs];
+  a.out_rows = out_rows;
+  a.d = pb->head_dim;
+  a.shared_idx = 1;
+  return hip_status(launch_compact(a, static_cast<hipStream_t>(stream)));
+}
+
 int stepkv_select(const stepkv_problem* pb, const float* scores, const uint8_t* protected_mask,
                   const int32_t* step_ids, int32_t budget, const int32_t* budgets, int32_t* idx,
                   int32_t* cu_retained, int32_t* kept_per_step, void* stream) {
@@ -426,6 +538,7 @@ int stepkv_compact(const stepkv_problem* pb, const void* k, const void* v, const
   a.ntot = pb->cu_seqlens_host[pb->num_seqs];
   a.out_rows = out_rows;
   a.d = pb->head_dim;
+  a.shared_idx = 0;
   return hip_status(launch_compact(a, static_cast<hipStream_t>(stream)));
 }
 

@@ -29,7 +29,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
     const int j = o - a.cu_retained[s];
     const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
     if (j < 0 || j >= ns) continue;
-    const int pos = a.idx[in_head + seq0 + j];
+    const int pos = a.idx[(a.shared_idx ? 0 : in_head) + seq0 + j];
     if (pos < 0 || pos >= ns) continue;  // not a valid position: row left untouched
     const size_t src = (in_head + seq0 + pos) * (size_t)D;
     const size_t dst = (out_head + o) * (size_t)D;

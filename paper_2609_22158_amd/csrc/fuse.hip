@@ -328,6 +328,29 @@ __global__ __launch_bounds__(kThreads) void fuse_stream_kernel(FuseArgs a) {
 
 }  // namespace
 
+namespace {
+
+// Shared-index mode: A_i = sum of the window saliency of `heads` (layer, KV
+// head) rows, added in row order (deterministic). Coalesced: consecutive
+// threads read consecutive tokens of each row.
+__global__ __launch_bounds__(256) void sum_heads_kernel(const float* __restrict__ sal, int heads,
+                                                        int ntot, float* __restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= ntot) return;
+  float acc = sal[i];
+  for (int h = 1; h < heads; ++h) acc += sal[(size_t)h * ntot + i];
+  out[i] = acc;
+}
+
+}  // namespace
+
+hipError_t launch_sum_heads(const float* sal, int heads, int ntot, float* out, hipStream_t st) {
+  if (ntot == 0 || heads == 0) return hipSuccess;
+  hipLaunchKernelGGL(sum_heads_kernel, dim3((ntot + 255) / 256), dim3(256), 0, st, sal, heads,
+                     ntot, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_fuse(const FuseArgs& a, hipStream_t st) {
   if (a.S * a.LH == 0) return hipSuccess;
   size_t dyn = (size_t)a.max_steps * 4;

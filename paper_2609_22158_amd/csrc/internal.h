@@ -49,6 +49,8 @@ struct FuseArgs {
   float alpha, beta;
 };
 hipError_t launch_fuse(const FuseArgs& a, hipStream_t st);
+// out[i] = sum over h < heads of sal[h][i] (fp32, [heads][ntot] -> [ntot]).
+hipError_t launch_sum_heads(const float* sal, int heads, int ntot, float* out, hipStream_t st);
 
 // ---------------------------------------------------------------- select
 struct SelectArgs {
@@ -69,12 +71,13 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t st);
 struct CompactArgs {
   const uint16_t* k;         // bf16 [L*Hkv][Ntot][d]
   const uint16_t* v;
-  const int32_t* idx;        // [L*Hkv][Ntot]
+  const int32_t* idx;        // [L*Hkv][Ntot], or [Ntot] shared by every head
   const int32_t* cu_seqlens; // [S+1]
   const int32_t* cu_retained;// [S+1]
   uint16_t* k_out;           // bf16 [L*Hkv][out_rows][d]
   uint16_t* v_out;
   int S, LH, ntot, out_rows, d;
+  int shared_idx;            // nonzero: one idx row for every (layer, KV head)
 };
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
 

@@ -132,13 +132,15 @@ __host__ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 // D: head dim. RG: row groups of 64 window rows (1, 2 or 4); the 4 / RG
-// waves per row group split each key tile into 32-key sub-tiles.
+// waves per row group split each key tile into 32-key sub-tiles. CAUSAL:
+// window slot w sees keys up to N_s - W + w only (the mask code exists only
+// in these instantiations).
 //
 // The tile loop is unrolled by the ring depth so that every ring slot is a
 // compile-time LDS offset: fragment reads use per-lane addresses computed
 // once plus an immediate, and full tiles load from a scalar base plus
 // per-lane constant offsets.
-template <int D, int RG, int PASS>
+template <int D, int RG, int PASS, bool CAUSAL>
 __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   constexpr int KG = 4 / RG;
   constexpr int TILE = 32 * KG;               // keys per workgroup iteration
@@ -288,7 +290,9 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   // i <= N_s - W + w. Only tiles reaching past N_s - W have hidden entries;
   // their logits become -inf, which every later step maps to probability 0.
   const int hidden_from = ns - a.W + 1;  // first key hidden from some window slot
-  auto tile_has_hidden = [&](int t) __attribute__((always_inline)) { return a.causal && key0 + (t + 1) * TILE > hidden_from; };
+  auto tile_has_hidden = [&](int t) __attribute__((always_inline)) {
+    return CAUSAL && key0 + (t + 1) * TILE > hidden_from;
+  };
   auto mask_hidden = [&](f32x16_t(&acc)[2], int t) __attribute__((always_inline)) {
     // key kin of the tile is visible to window row `row` iff kin <= lim + row / G
     const int lim = ns - a.W - key0 - t * TILE;
@@ -550,17 +554,36 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
 // no key get +inf, so that the second sweep gives them probability zero; the
 // natural-log value of every real row is exported when lse_out is set (-inf
 // for a row that sees no key).
-__global__ void lse_combine_kernel(SaliencyArgs a) {
+// 1024 threads per (sequence, head): each row's chunks are split over
+// 1024 / rows_pad groups, each taking a max pass then a sum pass of
+// independent loads, and the groups are merged in LDS.
+constexpr int kCombineThreads = 1024;
+
+__global__ __launch_bounds__(kCombineThreads) void lse_combine_kernel(SaliencyArgs a) {
+  __shared__ float2 part[kCombineThreads];
   const int LH = a.L * a.Hkv;
   const int s = blockIdx.x / LH, lh = blockIdx.x - s * LH;
-  const int row = threadIdx.x;
+  const int row = threadIdx.x % a.rows_pad, grp = threadIdx.x / a.rows_pad;
+  const int ngrp = kCombineThreads / a.rows_pad;
   const int c0 = a.cu_chunks[s], c1 = a.cu_chunks[s + 1];
-  float M = -INFINITY, Z = 0.f;
-  for (int c = c0; c < c1; ++c) {
-    const float2 p = a.partial[((size_t)lh * a.total_chunks + c) * a.rows_pad + row];
-    const float Mn = fmaxf(M, p.x);
+  const float2* __restrict__ pp = a.partial + (size_t)lh * a.total_chunks * a.rows_pad + row;
+  float M = -INFINITY;
+  for (int c = c0 + grp; c < c1; c += ngrp) M = fmaxf(M, pp[(size_t)c * a.rows_pad].x);
+  float Z = 0.f;
+  if (M != -INFINITY) {
+    for (int c = c0 + grp; c < c1; c += ngrp) {
+      const float2 p = pp[(size_t)c * a.rows_pad];
+      Z += p.y * exp2f(p.x - M);  // a chunk whose keys this row never saw: (-inf, 0) -> 0
+    }
+  }
+  part[threadIdx.x] = make_float2(M, Z);
+  __syncthreads();
+  if (grp != 0) return;
+  for (int g = 1; g < ngrp; ++g) {
+    const float2 o = part[g * a.rows_pad + row];
+    const float Mn = fmaxf(M, o.x);
     if (Mn != -INFINITY) {
-      Z = Z * exp2f(M - Mn) + p.y * exp2f(p.x - Mn);
+      Z = Z * exp2f(M - Mn) + o.y * exp2f(o.x - Mn);
       M = Mn;
     }
   }
@@ -592,19 +615,25 @@ __global__ void lse_import_kernel(SaliencyArgs a) {
   a.lse2[((size_t)s * LH + lh) * a.rows_pad + row] = l2;
 }
 
-template <int D, int RG>
-hipError_t launch_passes(const SaliencyArgs& a, SaliencyMode mode, hipStream_t st) {
+template <int D, int RG, bool C>
+hipError_t launch_passes_c(const SaliencyArgs& a, SaliencyMode mode, hipStream_t st) {
   const int LH = a.L * a.Hkv;
   const unsigned grid = (unsigned)LH * (unsigned)a.total_chunks;
   if (mode != SaliencyMode::kFromLse) {
-    hipLaunchKernelGGL((saliency_kernel<D, RG, 1>), dim3(grid), dim3(kThreads), 0, st, a);
-    hipLaunchKernelGGL(lse_combine_kernel, dim3(a.S * LH), dim3(a.rows_pad), 0, st, a);
+    hipLaunchKernelGGL((saliency_kernel<D, RG, 1, C>), dim3(grid), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL(lse_combine_kernel, dim3(a.S * LH), dim3(kCombineThreads), 0, st, a);
   } else {
     hipLaunchKernelGGL(lse_import_kernel, dim3(a.S * LH), dim3(a.rows_pad), 0, st, a);
   }
   if (mode != SaliencyMode::kLseOnly)
-    hipLaunchKernelGGL((saliency_kernel<D, RG, 2>), dim3(grid), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((saliency_kernel<D, RG, 2, C>), dim3(grid), dim3(kThreads), 0, st, a);
   return hipGetLastError();
+}
+
+template <int D, int RG>
+hipError_t launch_passes(const SaliencyArgs& a, SaliencyMode mode, hipStream_t st) {
+  return a.causal ? launch_passes_c<D, RG, true>(a, mode, st)
+                  : launch_passes_c<D, RG, false>(a, mode, st);
 }
 
 }  // namespace
@@ -619,7 +648,8 @@ hipError_t launch_saliency(const SaliencyArgs& a, int d, SaliencyMode mode, hipS
   if (e != hipSuccess) return e;
   if (a.total_chunks == 0) {  // no keys at all: every exported row LSE is -inf
     if (mode == SaliencyMode::kLseOnly)
-      hipLaunchKernelGGL(lse_combine_kernel, dim3(a.S * a.L * a.Hkv), dim3(a.rows_pad), 0, st, a);
+      hipLaunchKernelGGL(lse_combine_kernel, dim3(a.S * a.L * a.Hkv), dim3(kCombineThreads), 0, st,
+                         a);
     return hipGetLastError();
   }
   const int rg = a.rows_pad / 64;

@@ -31,7 +31,7 @@ def _declared_functions():
 
 def test_exports_every_declared_function(lib):
     names = _declared_functions()
-    assert len(names) == 15, names
+    assert len(names) == 19, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGNATURES)
@@ -210,3 +210,26 @@ def test_lse_entry_points_reject(lib):
     bad = _problem(W=65)
     assert lib.stepkv_saliency_from_lse(ctypes.byref(bad), R, FAKE, FAKE, FAKE, FAKE, FAKE * 16,
                                         need, None) == B.EUNSUPPORTED
+
+
+def test_step_tracker_incremental_matches_oracle(lib):
+    """Boundary-by-boundary updates (with a snapshot and restore in between) give the
+    oracle's utilities after every boundary."""
+    w = make_workload("l32_32k", 42, num_layers=1, with_v=False)
+    sig = w.signals[0]
+    n = sig.num_steps
+    tr = B.StepTracker(n)
+    snap = None
+    for t in range(n):
+        if t == n - 1:
+            snap = tr.snapshot()
+        S = tr.update(sig.valid[t], sig.gain[t], sig.red[t], sig.obs_sim[t, :t])
+        _, _, S_o = O.run_step_updates(sig.valid[:t + 1], sig.gain[:t + 1], sig.red[:t + 1],
+                                       sig.obs_sim[:t + 1, :t + 1].astype(np.float64), O.Params())
+        np.testing.assert_allclose(S, S_o, rtol=2e-7, atol=2e-7)
+    out = np.zeros(n, np.float32)
+    tr.restore(snap)
+    tr.update(sig.valid[n - 1], sig.gain[n - 1], sig.red[n - 1], sig.obs_sim[n - 1, :n - 1], out=out)
+    np.testing.assert_array_equal(out, S)
+    with pytest.raises(ValueError):
+        tr.update(1.0, 0.5, 0.0, np.zeros(3))  # wrong sim_prev length
