@@ -1,7 +1,10 @@
 // K/V compaction (eq. problem): C_hat = C_prot || C_traj[K], a bit-exact
 // gather of whole key/value rows into a dense retained cache, in position
 // order. One 16-byte piece per lane, whole rows per lane group, non-temporal
-// loads and stores (every byte is touched once).
+// loads and stores (every byte is touched once). One row per thread and many
+// small blocks keep the most bytes in flight (one 16-byte piece per thread is
+// also what a plain copy needs to approach the HBM ceiling on this part);
+// with several rows per thread, all index loads go first, then all K/V loads.
 #include "common.h"
 #include "internal.h"
 
@@ -9,7 +12,14 @@ namespace stepkv {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kRowsPerBlock = 64;
+#ifndef STEPKV_COMPACT_PASSES
+#define STEPKV_COMPACT_PASSES 1
+#endif
+constexpr int kPasses = STEPKV_COMPACT_PASSES;  // rows per thread
+
+// Rows one block gathers: a row is 2d bytes, 16 per lane.
+template <int D>
+constexpr int rows_per_block() { return kThreads / (2 * D / 16) * kPasses; }
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -17,39 +27,69 @@ template <int D>
 __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   constexpr int kLanesPerRow = 2 * D / 16;
   constexpr int kRowsPerPass = kThreads / kLanesPerRow;
+  constexpr int kRowsPerBlock = rows_per_block<D>();
   const int nb = (a.out_rows + kRowsPerBlock - 1) / kRowsPerBlock;
   const int lh = blockIdx.x / nb, rb = blockIdx.x - lh * nb;
   const int total = min(a.out_rows, a.cu_retained[a.S]);
-  const int r_end = min(total, (rb + 1) * kRowsPerBlock);
   const int sub = threadIdx.x / kLanesPerRow, piece = threadIdx.x % kLanesPerRow;
   const size_t in_head = (size_t)lh * a.ntot;
   const size_t out_head = (size_t)lh * a.out_rows;
-  for (int o = rb * kRowsPerBlock + sub; o < r_end; o += kRowsPerPass) {
-    const int s = segment_of(a.cu_retained, a.S, o);
-    const int j = o - a.cu_retained[s];
-    const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
-    if (j < 0 || j >= ns) continue;
-    const int pos = a.idx[(a.shared_idx ? 0 : in_head) + seq0 + j];
-    if (pos < 0 || pos >= ns) continue;  // not a valid position: row left untouched
-    const size_t src = (in_head + seq0 + pos) * (size_t)D;
+  const int32_t* __restrict__ idx = a.idx + (a.shared_idx ? 0 : in_head);
+  // 1. every row's source position (independent index loads). When the
+  // block's rows all belong to one sequence (always, but at sequence
+  // boundaries), that sequence is found once, in scalar registers.
+  const int o0 = rb * kRowsPerBlock;
+  const int s0 = uniform(segment_of(a.cu_retained, a.S, max(min(o0, total - 1), 0)));
+  const bool one_seq = o0 >= a.cu_retained[s0] && o0 + kRowsPerBlock <= a.cu_retained[s0 + 1];
+  int src_row[kPasses];
+  bool ok[kPasses];
+#pragma unroll
+  for (int p = 0; p < kPasses; ++p) {
+    const int o = o0 + p * kRowsPerPass + sub;
+    ok[p] = false;
+    src_row[p] = 0;
+    if (o < total) {
+      const int s = one_seq ? s0 : segment_of(a.cu_retained, a.S, o);
+      const int j = o - a.cu_retained[s];
+      const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
+      if (j < ns) {
+        const int pos = idx[seq0 + j];
+        ok[p] = pos >= 0 && pos < ns;  // not a valid position: row left untouched
+        src_row[p] = ok[p] ? seq0 + pos : 0;
+      }
+    }
+  }
+  // 2. all K/V pieces in flight at once (row 0 of the head stands in for skipped rows)
+  u32x4_t kv[kPasses], vv[kPasses];
+#pragma unroll
+  for (int p = 0; p < kPasses; ++p) {
+    const size_t src = (in_head + src_row[p]) * (size_t)D;
+    kv[p] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.k + src) + piece);
+    vv[p] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.v + src) + piece);
+  }
+  // 3. the dense retained rows
+#pragma unroll
+  for (int p = 0; p < kPasses; ++p) {
+    if (!ok[p]) continue;
+    const int o = rb * kRowsPerBlock + p * kRowsPerPass + sub;
     const size_t dst = (out_head + o) * (size_t)D;
-    const u32x4_t kv = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.k + src) + piece);
-    const u32x4_t vv = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(a.v + src) + piece);
-    __builtin_nontemporal_store(kv, reinterpret_cast<u32x4_t*>(a.k_out + dst) + piece);
-    __builtin_nontemporal_store(vv, reinterpret_cast<u32x4_t*>(a.v_out + dst) + piece);
+    __builtin_nontemporal_store(kv[p], reinterpret_cast<u32x4_t*>(a.k_out + dst) + piece);
+    __builtin_nontemporal_store(vv[p], reinterpret_cast<u32x4_t*>(a.v_out + dst) + piece);
   }
 }
 
 }  // namespace
 
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st) {
-  if (a.out_rows <= 0 || a.LH == 0) return hipSuccess;
-  const unsigned nb = (unsigned)((a.out_rows + kRowsPerBlock - 1) / kRowsPerBlock);
-  const dim3 grid((unsigned)a.LH * nb);
-  if (a.d == 128)
-    hipLaunchKernelGGL(compact_kernel<128>, grid, dim3(kThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL(compact_kernel<64>, grid, dim3(kThreads), 0, st, a);
+  // no tokens: nothing to gather (and no row 0 for skipped rows to stand on)
+  if (a.out_rows <= 0 || a.LH == 0 || a.ntot == 0) return hipSuccess;
+  if (a.d == 128) {
+    const unsigned nb = (unsigned)((a.out_rows + rows_per_block<128>() - 1) / rows_per_block<128>());
+    hipLaunchKernelGGL(compact_kernel<128>, dim3((unsigned)a.LH * nb), dim3(kThreads), 0, st, a);
+  } else {
+    const unsigned nb = (unsigned)((a.out_rows + rows_per_block<64>() - 1) / rows_per_block<64>());
+    hipLaunchKernelGGL(compact_kernel<64>, dim3((unsigned)a.LH * nb), dim3(kThreads), 0, st, a);
+  }
   return hipGetLastError();
 }
 
