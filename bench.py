@@ -69,9 +69,12 @@ SALIENCY_KERNELS = ("saliency_kernel", "lse_combine_kernel", "lse_import_kernel"
 def _saliency_part(name: str, lse_fed: bool):
     """The saliency-stage kernel a dispatch belongs to, or None. With lse_fed the
     row-LSE sweep and its combine belong to the untimed prefill stand-in."""
+    import re
+
     for k in SALIENCY_KERNELS:
         if k in name:
-            if lse_fed and (k == "lse_combine_kernel" or (k == "saliency_kernel" and ", 1>" in name)):
+            first_sweep = k == "saliency_kernel" and re.search(r"saliency_kernel<\d+, \d+, 1[,>]", name)
+            if lse_fed and (k == "lse_combine_kernel" or first_sweep):
                 return None
             return k
     return None
