@@ -3,9 +3,11 @@
 
 One step = the whole pass over one synthetic batch at one pruning boundary:
 host step-utility update for the newest step of every sequence (Algorithm 1
-phases 1-2, from the state of the boundaries before it) -> saliency ->
-priority -> top-B select -> K/V compaction, all layers and KV heads. Inputs
-are resident in HBM before the timed region. Prints one JSON line.
+phases 1-2, from the state of the boundaries before it; it runs on the host
+while the GPU computes the saliency, which does not depend on it) ->
+saliency -> priority -> top-B select -> K/V compaction, all layers and KV
+heads. Inputs are resident in HBM before the timed region. Prints one JSON
+line.
 
 By default the saliency is computed from the window queries and the cache
 alone (two sweeps over K). With --lse-fed the window rows' log-sum-exps are
@@ -51,6 +53,9 @@ def parse():
                     help="take the window rows' log-sum-exps as an input (one sweep over K)")
     ap.add_argument("--causal-tail", action="store_true",
                     help="window slot w sees keys up to N - W + w only (causal prefill)")
+    ap.add_argument("--text-signals", action="store_true",
+                    help="derive each boundary's step signals from synthetic trajectory text "
+                         "(host engine) instead of drawing them")
     ap.add_argument("--shared-layers", type=int, default=0,
                     help="shared-index mode: rank each sequence once from the saliency of its "
                          "last N layers and compact every layer and head with that one set")
@@ -277,7 +282,11 @@ def main():
     sid = torch.from_numpy(w.step_ids).to(dev)
     prot = torch.from_numpy(w.protected).to(dev)
     util = torch.empty(pb.total_steps, dtype=torch.float32, device=dev)
-    util_pinned = torch.empty(pb.total_steps, dtype=torch.float32, pin_memory=True)
+    # two pinned staging buffers, so that the host can fill one while the copy of
+    # the other may still be queued; an event per buffer marks its copy done
+    util_pinned = torch.empty((2, pb.total_steps), dtype=torch.float32, pin_memory=True)
+    copy_done = [torch.cuda.Event(), torch.cuda.Event()]
+    slot = [0]
     L, Hkv, ntot, d = w.num_layers, w.num_kv_heads, w.total_tokens, w.head_dim
     sal = torch.empty((L, Hkv, ntot), dtype=torch.float32, device=dev)
     scores = torch.empty_like(sal)
@@ -295,11 +304,20 @@ def main():
         torch.cuda.synchronize()
 
     # a0 state: every trajectory's step utilities up to the boundary before its last step
-    trackers, snaps = [], []
-    for g in w.signals:
-        tr = B.StepTracker(g.num_steps)
-        for t in range(g.num_steps - 1):
-            tr.update(g.valid[t], g.gain[t], g.red[t], g.obs_sim[t, :t])
+    trackers, snaps, texts = [], [], []
+    for i, g in enumerate(w.signals):
+        if args.text_signals:  # the signals come from each step's text
+            from synth.text import make_text_trajectory
+
+            steps = make_text_trajectory(args.seed + 7919 * i, g.num_steps)
+            tr = B.TextTracker(g.num_steps)
+            for t in range(g.num_steps - 1):
+                tr.update(*steps[t])
+            texts.append(steps[-1])
+        else:
+            tr = B.StepTracker(g.num_steps)
+            for t in range(g.num_steps - 1):
+                tr.update(g.valid[t], g.gain[t], g.red[t], g.obs_sim[t, :t])
         trackers.append(tr)
         snaps.append(tr.snapshot())
     util_host = util_pinned.numpy()
@@ -307,21 +325,28 @@ def main():
 
     def host_update():
         # a0: the boundary after each sequence's newest step (Algorithm 1 phases 1-2)
+        b = slot[0]
+        slot[0] ^= 1
+        copy_done[b].synchronize()  # the previous copy out of this buffer has run
         for i, (g, tr) in enumerate(zip(w.signals, trackers)):
             tr.restore(snaps[i])  # every timed step redoes the same boundary
-            t = g.num_steps - 1
-            tr.update(g.valid[t], g.gain[t], g.red[t], g.obs_sim[t, :t],
-                      out=util_host[cu_steps[i]:cu_steps[i + 1]])
-        util.copy_(util_pinned, non_blocking=True)
+            out = util_host[b, cu_steps[i]:cu_steps[i + 1]]
+            if args.text_signals:
+                tr.update(*texts[i], out=out)
+            else:
+                t = g.num_steps - 1
+                tr.update(g.valid[t], g.gain[t], g.red[t], g.obs_sim[t, :t], out=out)
+        util.copy_(util_pinned[b], non_blocking=True)
+        copy_done[b].record(stream)
 
     def step(ev=None):
-        host_update()
         if ev:
             ev[0].record(stream)
         if lse is None:
             B.saliency(pb, q, k, params, workspace=ws, out=sal)
         else:
             B.saliency_from_lse(pb, q, k, lse, params, workspace=ws, out=sal)
+        host_update()  # on the host while the GPU runs the saliency, which does not need S
         if ev:
             ev[1].record(stream)
         B.priority(pb, sal, sid, prot, util, params, scores=scores)
@@ -439,7 +464,9 @@ def main():
                                + (", row LSE given" if args.lse_fed else "")
                                + (", causal window" if args.causal_tail else "")
                                + (f", one ranking per sequence from the last {n_sh} layers"
-                                  if shared else ""),
+                                  if shared else "")
+                               + (", step signals from text" if args.text_signals else ""),
+                   "text_signals": bool(args.text_signals),
                    "shared_layers": n_sh if shared else 0,
                    "saliency_sweeps": sweeps, "causal_tail": bool(args.causal_tail),
                    "layers": L, "kv_heads": Hkv, "q_heads": w.num_q_heads, "head_dim": d,

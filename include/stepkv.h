@@ -77,6 +77,7 @@ extern "C" {
 #define STEPKV_MAX_WINDOW_ROWS 256   /* W * G */
 #define STEPKV_MAX_POOL_KERNEL 63    /* odd pooling window */
 #define STEPKV_MAX_STEPS_STATS 4096  /* steps per sequence when stats are requested */
+#define STEPKV_CUE_CAP 64            /* evidence cues per text field (App. D) */
 
 /* ---------------------------------------------------------------- types */
 /* Shape of one compression problem: a batch of S sequences, all layers. */
@@ -156,6 +157,47 @@ int64_t stepkv_budget_from_ratio(double rho, int64_t n_prunable);
  * similarity outside [0, 1] or non-finite signal. O(t), host only. */
 int stepkv_step_update(stepkv_step_state* state, float valid, float gain, float red,
                        const float* obs_sim_prev, const stepkv_params* prm, float* S_out);
+
+/* ---------------------------------------------------------------- step signals from text
+ * Sec. 5.1.1 (observation validity, evidence gain, action redundancy) and the
+ * observation similarities of the reuse update (eq. reuse, Sec. 5.1.2),
+ * computed on the host from each step's Thought, Action and Observation text.
+ * The paper's sim is an overlap of at most STEPKV_CUE_CAP extracted evidence
+ * cues per field (App. D); here:
+ *  - a cue is a maximal run of ASCII letters and digits (other bytes, UTF-8
+ *    included, separate cues), lowercased, of two or more bytes, and not a
+ *    common English function word; a field keeps its distinct cues in order
+ *    of first appearance, the first STEPKV_CUE_CAP;
+ *  - sim(a, b) = |A & B| / |A | B| (0 when both are empty);
+ *  - valid = 0 when the observation has no cue or starts (after ASCII
+ *    whitespace, case-insensitively) with an error marker: "error",
+ *    "exception", "traceback", "invalid", "failed", "failure", "no results",
+ *    "not found", "timed out", "timeout";
+ *  - gain_k = 1 - max_{u<k} sim(Th_k || Obs_k, Th_u || Obs_u), gain_1 = 1;
+ *    red_k = max_{u<k} sim(Act_k, Act_u), red_1 = 0.
+ * The trajectory's state is caller-owned host memory (8-byte aligned) of
+ * stepkv_text_state_bytes(capacity) bytes; texts are (pointer, length) pairs
+ * of bytes, not necessarily NUL-terminated. The outputs feed
+ * stepkv_step_update for the same boundary. Host-only; O(t) per boundary. */
+
+/* Bytes of host state for a trajectory of up to `capacity` steps (0 if < 1). */
+size_t stepkv_text_state_bytes(int32_t capacity);
+
+/* Initialise (or reset) a trajectory's text state. EINVAL: null or misaligned
+ * state, capacity < 1 or bytes too small. */
+int stepkv_text_state_init(void* state, size_t bytes, int32_t capacity);
+
+/* Add step t (the t-th call since init): extract its cues, write valid, gain,
+ * red and obs_sim_prev[k] = sim(Obs_t, Obs_k) for k < t (t floats; may be
+ * NULL when t = 0). EINVAL: null outputs, an uninitialised or full state, a
+ * negative length or a NULL text with a positive length. */
+int stepkv_text_step(void* state, const char* thought, int64_t thought_len, const char* action,
+                     int64_t action_len, const char* observation, int64_t observation_len,
+                     float* valid, float* gain, float* red, float* obs_sim_prev);
+
+/* The cues of one text as 64-bit FNV-1a hashes of their lowercased bytes, in
+ * order of first appearance: cues[0 .. *count), *count <= STEPKV_CUE_CAP. */
+int stepkv_text_cues(const char* text, int64_t text_len, uint64_t* cues, int32_t* count);
 
 /* ---------------------------------------------------------------- device passes */
 /* Bytes of device workspace stepkv_score needs for this problem (0 when the

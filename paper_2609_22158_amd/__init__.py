@@ -11,6 +11,7 @@ from .binding import (  # noqa: F401
     Problem,
     StepKVError,
     StepTracker,
+    TextTracker,
     budget_from_ratio,
     compact,
     compact_shared,
@@ -27,5 +28,6 @@ from .binding import (  # noqa: F401
     select,
     select_shared,
     step_utilities,
+    text_cues,
     window_lse,
 )

@@ -16,6 +16,7 @@ import numpy as np
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstepkv.so")
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
+CUE_CAP = 64  # STEPKV_CUE_CAP
 MAX_WINDOW_ROWS = 256
 MAX_POOL_KERNEL = 63
 MAX_STEPS_STATS = 4096
@@ -82,6 +83,14 @@ _SIGNATURES = {
     "stepkv_step_update": (ctypes.c_int, [ctypes.POINTER(StepStateC), ctypes.c_float,
                                           ctypes.c_float, ctypes.c_float, _f32p,
                                           ctypes.POINTER(ParamsC), _f32p]),
+    "stepkv_text_state_bytes": (ctypes.c_size_t, [ctypes.c_int32]),
+    "stepkv_text_state_init": (ctypes.c_int, [_vp, ctypes.c_size_t, ctypes.c_int32]),
+    "stepkv_text_step": (ctypes.c_int, [_vp, ctypes.c_char_p, ctypes.c_int64, ctypes.c_char_p,
+                                        ctypes.c_int64, ctypes.c_char_p, ctypes.c_int64, _f32p,
+                                        _f32p, _f32p, _f32p]),
+    "stepkv_text_cues": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_int64,
+                                        ctypes.POINTER(ctypes.c_uint64),
+                                        ctypes.POINTER(ctypes.c_int32)]),
     "stepkv_score_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
     "stepkv_saliency_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
     "stepkv_saliency": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp,
@@ -252,6 +261,61 @@ class StepTracker:
         self.r[:] = r
         self.c[:] = c
         self._st.num_steps = n
+
+
+def _text(x) -> bytes:
+    return x if isinstance(x, bytes) else str(x).encode("utf-8")
+
+
+def text_cues(text) -> np.ndarray:
+    """stepkv_text_cues: the cues of one text as uint64 FNV-1a hashes, in order."""
+    data = _text(text)
+    out = (ctypes.c_uint64 * CUE_CAP)()
+    n = ctypes.c_int32(0)
+    _check("stepkv_text_cues", load().stepkv_text_cues(data, len(data), out, ctypes.byref(n)))
+    return np.array(out[:n.value], dtype=np.uint64)
+
+
+class TextTracker:
+    """Step signals of one trajectory from its text (stepkv_text_step), optionally fed
+    straight into the utilities (StepTracker): `signals` adds a step and returns
+    (valid, gain, red, obs_sim_prev); `update` also advances the utilities and returns S."""
+
+    def __init__(self, capacity: int, params: Optional[Params] = None):
+        lib = load()
+        self.capacity = max(int(capacity), 1)
+        nbytes = int(lib.stepkv_text_state_bytes(self.capacity))
+        self._nbytes = nbytes
+        self._state = np.zeros((nbytes + 7) // 8, np.uint64)  # 8-byte aligned host memory
+        _check("stepkv_text_state_init",
+               lib.stepkv_text_state_init(self._state.ctypes.data, nbytes, self.capacity))
+        self.steps = StepTracker(self.capacity, params)
+        self._sim = np.zeros(self.capacity, np.float32)
+
+    @property
+    def num_steps(self) -> int:
+        return int(self._state[:2].view(np.int32)[2])  # the state header's step count
+
+    def signals(self, thought, action, observation):
+        t = self.num_steps
+        th, ac, ob = _text(thought), _text(action), _text(observation)
+        v, g, r = ctypes.c_float(), ctypes.c_float(), ctypes.c_float()
+        rc = load().stepkv_text_step(self._state.ctypes.data, th, len(th), ac, len(ac), ob, len(ob),
+                                     ctypes.byref(v), ctypes.byref(g), ctypes.byref(r),
+                                     self._sim.ctypes.data_as(_f32p))
+        _check("stepkv_text_step", rc)
+        return v.value, g.value, r.value, self._sim[:t].copy()
+
+    def update(self, thought, action, observation, out=None) -> np.ndarray:
+        v, g, r, sim = self.signals(thought, action, observation)
+        return self.steps.update(v, g, r, sim, out=out)
+
+    def snapshot(self):
+        return self._state.copy(), self.steps.snapshot()
+
+    def restore(self, snap) -> None:
+        self._state[:] = snap[0]
+        self.steps.restore(snap[1])
 
 
 # ---------------------------------------------------------------- problem

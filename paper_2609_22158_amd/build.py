@@ -16,7 +16,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libstepkv.so")
 
-SOURCES = ["api.cpp", "saliency.hip", "fuse.hip", "select.hip", "compact.hip", "decode.hip"]
+SOURCES = ["api.cpp", "step_text.cpp", "saliency.hip", "fuse.hip", "select.hip", "compact.hip",
+           "decode.hip"]
 ARCH = "gfx950"
 
 
