@@ -56,6 +56,12 @@ def parse():
     ap.add_argument("--text-signals", action="store_true",
                     help="derive each boundary's step signals from synthetic trajectory text "
                          "(host engine) instead of drawing them")
+    ap.add_argument("--decode", action="store_true",
+                    help="add one decode step over the compacted cache (every layer and query "
+                         "head, random queries) to each step, as its own stage")
+    ap.add_argument("--selector", choices=("stepkv", "token-only", "last-query"), default="stepkv",
+                    help="token-only: the pooled window saliency alone (beta = 0, SnapKV-style); "
+                         "last-query: one window query, no pooling, beta = 0 (TOVA-style)")
     ap.add_argument("--shared-layers", type=int, default=0,
                     help="shared-index mode: rank each sequence once from the saliency of its "
                          "last N layers and compact every layer and head with that one set")
@@ -188,7 +194,8 @@ def cpu_baseline(w, budget, seconds, params, lse_fed=False):
                for s in range(w.num_seqs)]
     rng = np.random.default_rng(0)
     rng.shuffle(triples)
-    op = O.Params(causal_tail=bool(params.causal_tail))
+    op = O.Params(alpha=params.alpha, beta=params.beta, pool_kernel=params.pool_kernel,
+                  causal_tail=bool(params.causal_tail))
     G = w.num_q_heads // w.num_kv_heads
     lse_win = np.zeros(w.q_win.shape[:4]) if lse_fed else None
     done, tokens, dt = 0, 0, 0.0
@@ -229,7 +236,8 @@ def cpu_baseline_shared(w, budget, seconds, params, last_layers):
         threads = 1
     S = np.concatenate([O.run_step_updates(g.valid, g.gain, g.red, g.obs_sim.astype(np.float64),
                                            O.Params())[2] for g in w.signals])
-    op = O.Params(causal_tail=bool(params.causal_tail))
+    op = O.Params(alpha=params.alpha, beta=params.beta, pool_kernel=params.pool_kernel,
+                  causal_tail=bool(params.causal_tail))
     done, tokens, dt = 0, 0, 0.0
     for s in range(w.num_seqs):
         t0 = time.perf_counter()
@@ -264,6 +272,8 @@ def main():
     kw = {}
     if args.window:
         kw["window"] = args.window
+    if args.selector == "last-query":
+        kw["window"] = 1
     if args.layers:
         kw["num_layers"] = args.layers
     w = make_workload(args.workload, args.seed, **kw)
@@ -296,7 +306,12 @@ def main():
     k_out = torch.empty((L, Hkv, out_rows, d), dtype=torch.bfloat16, device=dev)
     v_out = torch.empty_like(k_out)
     ws = torch.empty(pb.saliency_workspace_bytes(), dtype=torch.uint8, device=dev)
-    params = B.Params(causal_tail=int(args.causal_tail))
+    if args.selector == "token-only":
+        params = B.Params.token_only(causal_tail=int(args.causal_tail))
+    elif args.selector == "last-query":
+        params = B.Params.last_query_only(causal_tail=int(args.causal_tail))
+    else:
+        params = B.Params(causal_tail=int(args.causal_tail))
     stream = torch.cuda.current_stream()
     lse = None
     if args.lse_fed:  # stands for the prefill attention's row LSE, resident in HBM
@@ -339,6 +354,23 @@ def main():
         util.copy_(util_pinned[b], non_blocking=True)
         copy_done[b].record(stream)
 
+    if args.decode:  # one decode query per (layer, sequence, query head)
+        qd_bits = np.random.default_rng(args.seed + 1).standard_normal(
+            (L, w.num_seqs, w.num_q_heads, d)).astype(np.float32)
+        from synth import f32_to_bf16_bits
+
+        q_dec = B.bf16_from_bits(f32_to_bf16_bits(qd_bits), dev)
+        dec_out = torch.empty((L, w.num_seqs, w.num_q_heads, d), dtype=torch.float32, device=dev)
+        dec_ws = torch.empty(max(int(B.load().stepkv_decode_workspace_bytes(
+            B.ctypes.byref(pb.c), out_rows)), 1), dtype=torch.uint8, device=dev)
+
+    def decode(ev, i):
+        if args.decode:
+            B.decode_attention(pb, q_dec, k_out, v_out, cu_ret, out_rows, workspace=dec_ws,
+                               out=dec_out)
+            if ev:
+                ev[i].record(stream)
+
     def step(ev=None):
         if ev:
             ev[0].record(stream)
@@ -358,6 +390,7 @@ def main():
         B.compact(pb, k, v, idx, cu_ret, out_rows, k_out=k_out, v_out=v_out)
         if ev:
             ev[4].record(stream)
+        decode(ev, 5)
 
     shared = args.shared_layers > 0
     if shared:
@@ -381,6 +414,7 @@ def main():
             B.compact_shared(pb, k, v, idx_sh, cu_ret, out_rows, k_out=k_out, v_out=v_out)
             if ev:
                 ev[3].record(stream)
+            decode(ev, 4)
 
     for _ in range(args.warmup):
         step()
@@ -396,6 +430,8 @@ def main():
 
     stage_names = (["score", "select", "compact"] if shared
                    else ["saliency", "priority", "select", "compact"])
+    if args.decode:
+        stage_names.append("decode")
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stage_names) + 1)]
            for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
@@ -451,6 +487,11 @@ def main():
            "compact_gbps": round(compact_bytes / t_cmp / 1e9, 1),
            "compact_frac": round(compact_bytes / t_cmp / 1e9 / HBM_PEAK_GBS, 4),
            "peak_gbps": HBM_PEAK_GBS}
+    if args.decode:  # K_hat and V_hat read once (plus queries and outputs)
+        dec_bytes = lh * out_rows * d * 2 * 2 + q_dec.numel() * 2 + dec_out.numel() * 4
+        t_dec = stage_ms["decode"] * 1e-3
+        hbm.update({"decode_gbps": round(dec_bytes / t_dec / 1e9, 1),
+                    "decode_frac": round(dec_bytes / t_dec / 1e9 / HBM_PEAK_GBS, 4)})
 
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
@@ -465,7 +506,10 @@ def main():
                                + (", causal window" if args.causal_tail else "")
                                + (f", one ranking per sequence from the last {n_sh} layers"
                                   if shared else "")
-                               + (", step signals from text" if args.text_signals else ""),
+                               + (", step signals from text" if args.text_signals else "")
+                               + (f", {args.selector} selector" if args.selector != "stepkv"
+                                  else ""),
+                   "selector": args.selector,
                    "text_signals": bool(args.text_signals),
                    "shared_layers": n_sh if shared else 0,
                    "saliency_sweeps": sweeps, "causal_tail": bool(args.causal_tail),

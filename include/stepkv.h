@@ -358,14 +358,22 @@ int stepkv_compact(const stepkv_problem* pb, const void* k, const void* v, const
                    const int32_t* cu_retained, int32_t out_rows, void* k_out, void* v_out,
                    void* stream);
 
-/* One decode step over a compacted cache, to check that the compacted cache
- * is usable: for every layer l, sequence s and query head hq (KV head
- * hq / G), out = softmax(scale * q . K_hat^T) V_hat over the R_s rows of s.
- * q_dec bf16 [L][S][Hq][d]; out fp32 [L][S][Hq][d]; scale <= 0 selects
- * 1/sqrt(d). Errors: EINVAL, EUNSUPPORTED (d), EHIP. */
+/* Bytes of device workspace stepkv_decode_attention needs (0 when invalid). */
+size_t stepkv_decode_workspace_bytes(const stepkv_problem* pb, int32_t out_rows);
+
+/* One decode step over a compacted cache (Sec. 3: the compacted cache serves
+ * the next decoding steps): for every layer l, sequence s and query head hq
+ * (KV head hq / G), out = softmax(scale * q . K_hat^T) V_hat over the R_s
+ * rows of s (R_s from cu_retained, within out_rows). q_dec bf16 [L][S][Hq][d];
+ * out fp32 [L][S][Hq][d] (zero for a sequence with no row); scale <= 0
+ * selects 1/sqrt(d). Each KV head's rows are read once for its whole query
+ * group, split over workgroups of 512 rows. Errors: EINVAL, EUNSUPPORTED
+ * (d), EWORKSPACE (below stepkv_decode_workspace_bytes, or not 256-byte
+ * aligned), EHIP. */
 int stepkv_decode_attention(const stepkv_problem* pb, const void* q_dec, const void* k_hat,
                             const void* v_hat, const int32_t* cu_retained, int32_t out_rows,
-                            float scale, float* out, void* stream);
+                            float scale, float* out, void* workspace, size_t ws_bytes,
+                            void* stream);
 
 #ifdef __cplusplus
 }

@@ -119,8 +119,10 @@ _SIGNATURES = {
                                      _vp, _vp, _vp, _vp, _vp]),
     "stepkv_compact": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, _vp, _vp, _vp,
                                       ctypes.c_int32, _vp, _vp, _vp]),
+    "stepkv_decode_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC), ctypes.c_int32]),
     "stepkv_decode_attention": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, _vp, _vp, _vp,
-                                               ctypes.c_int32, ctypes.c_float, _vp, _vp]),
+                                               ctypes.c_int32, ctypes.c_float, _vp, _vp,
+                                               ctypes.c_size_t, _vp]),
 }
 
 _lib: Optional[ctypes.CDLL] = None
@@ -183,6 +185,19 @@ class Params:
 
     def c(self) -> ParamsC:
         return ParamsC(*[getattr(self, f) for f, _ in ParamsC._fields_])
+
+    @staticmethod
+    def token_only(pool_kernel: int = 7, **kw) -> "Params":
+        """A token-only selector on the same pass: the retention priority is the pooled
+        window saliency alone (beta = 0), as in the paper's 'w/o step score' ablation
+        (Table 3). With the default window this is a SnapKV-style selector."""
+        return Params(alpha=1.0, beta=0.0, pool_kernel=pool_kernel, **kw)
+
+    @staticmethod
+    def last_query_only(**kw) -> "Params":
+        """The TOVA-style selector: with a window of one query (W = 1 in the problem),
+        no pooling and beta = 0, tokens rank by the newest query's attention."""
+        return Params(alpha=1.0, beta=0.0, pool_kernel=1, **kw)
 
     @staticmethod
     def library_default() -> "Params":
@@ -668,7 +683,7 @@ def compact(pb: Problem, k, v, idx, cu_retained, out_rows: int, *, k_out=None, v
 
 
 def decode_attention(pb: Problem, q_dec, k_hat, v_hat, cu_retained, out_rows: int,
-                     scale: float = 0.0, stream=None):
+                     scale: float = 0.0, *, workspace=None, out=None, stream=None):
     """stepkv_decode_attention: fp32 [L][S][Hq][d]."""
     import torch
 
@@ -678,9 +693,15 @@ def decode_attention(pb: Problem, q_dec, k_hat, v_hat, cu_retained, out_rows: in
     kp = _need(k_hat, torch.bfloat16, (L, Hkv, out_rows, d), "k_hat")
     vp = _need(v_hat, torch.bfloat16, (L, Hkv, out_rows, d), "v_hat")
     cp = _need(cu_retained, torch.int32, (S + 1,), "cu_retained")
-    out = torch.empty((L, S, Hq, d), dtype=torch.float32, device=pb.device)
+    if out is None:
+        out = torch.empty((L, S, Hq, d), dtype=torch.float32, device=pb.device)
+    _need(out, torch.float32, (L, S, Hq, d), "out")
+    if workspace is None:
+        need = int(lib.stepkv_decode_workspace_bytes(ctypes.byref(pb.c), int(out_rows)))
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=pb.device)
     rc = lib.stepkv_decode_attention(ctypes.byref(pb.c), qp, kp, vp, cp, int(out_rows),
-                                     float(scale), out.data_ptr(), _stream(stream))
+                                     float(scale), out.data_ptr(), workspace.data_ptr(),
+                                     workspace.numel(), _stream(stream))
     _check("stepkv_decode_attention", rc)
     return out
 

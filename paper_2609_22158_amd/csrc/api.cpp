@@ -542,19 +542,35 @@ int stepkv_compact(const stepkv_problem* pb, const void* k, const void* v, const
   return hip_status(launch_compact(a, static_cast<hipStream_t>(stream)));
 }
 
+size_t stepkv_decode_workspace_bytes(const stepkv_problem* pb, int32_t out_rows) {
+  if (check_problem(pb) != STEPKV_OK || out_rows < 0) return 0;
+  DecodeArgs a{};
+  a.L = pb->num_layers;
+  a.Hkv = pb->num_kv_heads;
+  a.G = pb->num_q_heads / pb->num_kv_heads;
+  a.d = pb->head_dim;
+  a.total_splits = decode_total_splits(pb->cu_seqlens_host, pb->num_seqs, out_rows);
+  return std::max<size_t>(sizeof(float) * decode_partial_floats(a), kAlign);
+}
+
 int stepkv_decode_attention(const stepkv_problem* pb, const void* q_dec, const void* k_hat,
                             const void* v_hat, const int32_t* cu_retained, int32_t out_rows,
-                            float scale, float* out, void* stream) {
+                            float scale, float* out, void* workspace, size_t ws_bytes,
+                            void* stream) {
   const int rc = check_problem(pb);
   if (rc != STEPKV_OK) return rc;
   if (!q_dec || !k_hat || !v_hat || !cu_retained || !out || out_rows < 0 || !std::isfinite(scale))
     return STEPKV_EINVAL;
+  if (!workspace || ws_bytes < stepkv_decode_workspace_bytes(pb, out_rows) || !aligned(workspace))
+    return STEPKV_EWORKSPACE;
   DecodeArgs a;
   a.q = static_cast<const uint16_t*>(q_dec);
   a.k = static_cast<const uint16_t*>(k_hat);
   a.v = static_cast<const uint16_t*>(v_hat);
   a.cu_retained = cu_retained;
   a.out = out;
+  a.cu_seqlens = pb->cu_seqlens;
+  a.partial = static_cast<float*>(workspace);
   a.L = pb->num_layers;
   a.S = pb->num_seqs;
   a.Hq = pb->num_q_heads;
@@ -562,6 +578,7 @@ int stepkv_decode_attention(const stepkv_problem* pb, const void* q_dec, const v
   a.G = pb->num_q_heads / pb->num_kv_heads;
   a.d = pb->head_dim;
   a.out_rows = out_rows;
+  a.total_splits = decode_total_splits(pb->cu_seqlens_host, pb->num_seqs, out_rows);
   a.scale = scale > 0.0f ? scale : (float)(1.0 / std::sqrt((double)pb->head_dim));
   return hip_status(launch_decode(a, static_cast<hipStream_t>(stream)));
 }

@@ -88,9 +88,15 @@ struct DecodeArgs {
   const uint16_t* v;
   const int32_t* cu_retained;// [S+1]
   float* out;                // [L][S][Hq][d]
-  int L, S, Hq, Hkv, G, d, out_rows;
+  const int32_t* cu_seqlens; // [S+1]
+  float* partial;            // workspace: [L*Hkv][total_splits][G][d+2] (o, m, z)
+  int L, S, Hq, Hkv, G, d, out_rows, total_splits;
   float scale;
 };
+// Row splits of the split kernel for these sequence lengths and out_rows.
+int decode_total_splits(const int32_t* cu_seqlens_host, int S, int out_rows);
+// Floats of partial state the launch needs (0 for groups above 8 heads).
+size_t decode_partial_floats(const DecodeArgs& a);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t st);
 
 }  // namespace stepkv

@@ -31,7 +31,7 @@ def _declared_functions():
 
 def test_exports_every_declared_function(lib):
     names = _declared_functions()
-    assert len(names) == 23, names
+    assert len(names) == 24, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGNATURES)
@@ -184,9 +184,15 @@ def test_select_compact_decode_reject(lib):
     assert lib.stepkv_compact(ctypes.byref(pb), FAKE, None, FAKE, FAKE, 8, FAKE, FAKE,
                               None) == B.EINVAL
     assert lib.stepkv_decode_attention(ctypes.byref(_problem(d=80)), FAKE, FAKE, FAKE, FAKE, 8,
-                                       0.0, FAKE, None) == B.EUNSUPPORTED
+                                       0.0, FAKE, FAKE * 16, 1 << 20, None) == B.EUNSUPPORTED
+    need = lib.stepkv_decode_workspace_bytes(ctypes.byref(pb), 8)
+    assert need > 0
+    assert lib.stepkv_decode_attention(ctypes.byref(pb), FAKE, FAKE, FAKE, FAKE, 8, 0.0, FAKE,
+                                       FAKE * 16, need - 1, None) == B.EWORKSPACE
+    assert lib.stepkv_decode_attention(ctypes.byref(pb), FAKE, FAKE, FAKE, FAKE, 8, 0.0, None,
+                                       FAKE * 16, need, None) == B.EINVAL
     assert lib.stepkv_decode_attention(ctypes.byref(pb), FAKE, FAKE, FAKE, FAKE, 8,
-                                       float("inf"), FAKE, None) == B.EINVAL
+                                       float("inf"), FAKE, FAKE * 16, 1 << 20, None) == B.EINVAL
 
 
 def test_lse_entry_points_reject(lib):

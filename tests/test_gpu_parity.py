@@ -222,6 +222,31 @@ def test_single_signal_special_cases(alpha, beta):
         swap_ok(idx[l, h, :rows[0]], o["idx"][(s, l, h)], o["P"][(s, l, h)], prun, g.budget)
 
 
+@pytest.mark.parametrize("selector", ["token_only", "last_query_only"])
+def test_token_only_selectors(selector):
+    """Token-only selectors on the same kernels (beta = 0): SnapKV-style (window saliency,
+    pooled) and TOVA-style (one window query, no pooling), against the oracle, with the
+    selection bit-exact on the oracle's fp32 priorities."""
+    import torch
+
+    from paper_2609_22158_amd import binding as B
+
+    w = reduced("l1_8k", seqlens=[3001, 700], window=1 if selector == "last_query_only" else 32)
+    p = getattr(B.Params, selector)()
+    g = GpuRun(w, params=p)
+    log(f"[{selector}] W={w.window} pool={p.pool_kernel}")
+    sc = g.score(want_saliency=True)
+    o = run_oracle(w, g.budget, p)
+    P = sc["scores"].cpu().numpy()
+    A = sc["saliency"].cpu().numpy()
+    for s, l, h, a, b in _heads(w):
+        close(A[l, h, a:b], o["A"][(s, l, h)], f"A{(s, l, h)}")
+        close(P[l, h, a:b], o["P"][(s, l, h)], f"P{(s, l, h)}")
+    P32, Pdev = _oracle_scores_fp32(w, o)
+    idx, cu, _ = g.select(Pdev)
+    _check_selection(w, g, P32, idx.cpu().numpy(), cu.cpu().numpy(), None)
+
+
 def test_repeat_runs_are_bitwise_identical():
     """Fixed reduction orders: repeated runs give identical bits (idx only where defined)."""
     import torch
