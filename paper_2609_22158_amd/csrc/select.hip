@@ -131,8 +131,26 @@ __global__ __launch_bounds__(kThreads) void retained_plan_kernel(SelectArgs a) {
   if (threadIdx.x == 0) a.cu_retained[0] = 0;
   for (int s = 0; s < a.S; ++s) {
     const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
+    // protected flags counted 16 at a time from aligned 16-byte words; the
+    // unaligned head and tail one byte at a time
+    const int misal = (int)(reinterpret_cast<uintptr_t>(a.prot + seq0) & 15);
+    const int head = min(ns, (16 - misal) & 15);
+    const int nvec = (ns - head) / 16;
     int np = 0;
-    for (int i = threadIdx.x; i < ns; i += kThreads) np += a.prot[seq0 + i] != 0;
+    if ((int)threadIdx.x < head) np += a.prot[seq0 + threadIdx.x] != 0;
+    const uint4* vp = reinterpret_cast<const uint4*>(a.prot + seq0 + head);
+    for (int i = threadIdx.x; i < nvec; i += kThreads) {
+      const uint4 w = vp[i];
+      const uint32_t x[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {  // one bit per nonzero byte
+        uint32_t b = x[c] | (x[c] >> 4);
+        b |= b >> 2;
+        b |= b >> 1;
+        np += __builtin_popcount(b & 0x01010101u);
+      }
+    }
+    for (int i = head + 16 * nvec + threadIdx.x; i < ns; i += kThreads) np += a.prot[seq0 + i] != 0;
     np = block_sum_int(np, scratch);
     const int B = a.budgets ? max(1, a.budgets[s]) : a.budget;
     acc += np + min(B, ns - np);
