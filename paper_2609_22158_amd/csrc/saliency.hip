@@ -398,7 +398,33 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     nxt[0] = f32x16_t{};
     nxt[1] = f32x16_t{};
     float p4[2][4];
-    static_for<0, 2 * KSTEPS>([&](auto i2c) __attribute__((always_inline)) {
+    // The softmax work of slice s runs as three stages one MFMA apart (the
+    // scaled logit after MFMA s, its exp2 after MFMA s+1, the sum after MFMA
+    // s+2), so no VALU instruction waits on one issued just before it.
+    float lg[2][PER], ex[2][PER];
+    auto stage_logit = [&](auto sc) __attribute__((always_inline)) {
+      constexpr int sl = decltype(sc)::value;
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        const int e = sl * PER + q, bb = e >> 4, j = e & 15;
+        lg[sl & 1][q] = fmaf(cur[bb][j], a.c, -(PASS == 1 ? m2[bb] : lr[bb][j]));
+      }
+    };
+    auto stage_exp = [&](auto sc) __attribute__((always_inline)) {
+      constexpr int sl = decltype(sc)::value;
+#pragma unroll
+      for (int q = 0; q < PER; ++q) ex[sl & 1][q] = fast_exp2(lg[sl & 1][q]);
+    };
+    auto stage_sum = [&](auto sc) __attribute__((always_inline)) {
+      constexpr int sl = decltype(sc)::value;
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        const int e = sl * PER + q, bb = e >> 4, j = e & 15;
+        p4[bb][j & 3] = j < 4 ? ex[sl & 1][q] : p4[bb][j & 3] + ex[sl & 1][q];  // first touch needs no add
+      }
+    };
+    constexpr int NSL = 2 * KSTEPS;  // slices, one per MFMA
+    static_for<0, NSL>([&](auto i2c) __attribute__((always_inline)) {
       constexpr int i2 = decltype(i2c)::value;
       constexpr int st = i2 >> 1, b = i2 & 1;
       if constexpr (b == 0) lds_wait<KSTEPS - 1 - st>(kf[st]);
@@ -407,15 +433,14 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
       else
         nxt[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[b][st], kf[st], nxt[b], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int e = i2 * PER; e < (i2 + 1) * PER; ++e) {
-        const int bb = e >> 4, j = e & 15;
-        const float ref = PASS == 1 ? m2[bb] : lr[bb][j];
-        const float p = fast_exp2(fmaf(cur[bb][j], a.c, -ref));
-        p4[bb][j & 3] = j < 4 ? p : p4[bb][j & 3] + p;  // first touch needs no add
-      }
+      if constexpr (i2 >= 2) stage_sum(std::integral_constant<int, i2 - 2>{});
+      if constexpr (i2 >= 1) stage_exp(std::integral_constant<int, i2 - 1>{});
+      stage_logit(i2c);
       __builtin_amdgcn_sched_barrier(0);
     });
+    stage_exp(std::integral_constant<int, NSL - 1>{});
+    stage_sum(std::integral_constant<int, NSL - 2>{});
+    stage_sum(std::integral_constant<int, NSL - 1>{});
     if (PASS == 1) {
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
