@@ -17,7 +17,10 @@ using namespace stepkv;
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr int kMinItems = 2048;  // saliency work items wanted: ~8 per CU on 256 CUs
+#ifndef STEPKV_SAL_MIN_ITEMS
+#define STEPKV_SAL_MIN_ITEMS 2048
+#endif
+constexpr int kMinItems = STEPKV_SAL_MIN_ITEMS;  // saliency work items wanted: ~8 per CU on 256 CUs
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -74,7 +77,7 @@ SaliencyPlan plan_saliency(const stepkv_problem* pb) {
   // largest chunk that still gives enough workgroups; all are multiples of
   // every key tile (32, 64, 128)
   p.chunk = 256;
-  for (int c : {4096, 2048, 1024, 512}) {
+  for (int c : {16384, 8192, 4096, 2048, 1024, 512}) {
     if (lh * chunks_for(c) >= kMinItems) {
       p.chunk = c;
       break;

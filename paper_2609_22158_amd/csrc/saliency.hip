@@ -398,22 +398,32 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     nxt[0] = f32x16_t{};
     nxt[1] = f32x16_t{};
     float p4[2][4];
-    // The softmax work of slice s runs as three stages one MFMA apart (the
-    // scaled logit after MFMA s, its exp2 after MFMA s+1, the sum after MFMA
-    // s+2), so no VALU instruction waits on one issued just before it.
-    float lg[2][PER], ex[2][PER];
+    // pass-1 reference of this tile: m2, or 0 while m2 is -inf (then every key
+    // of this lane is hidden, in this tile and all later ones: the causal
+    // limit is a prefix of the keys and tile 0 set m2 from its visible keys)
+    float ref1[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) ref1[b] = m2[b] == -INFINITY ? 0.f : m2[b];
+    // The softmax work of slice s runs in three stages one MFMA apart: the
+    // scaled logit (in place in `cur`) after MFMA s, its exp2 after MFMA s+1
+    // and the sum after MFMA s+2, so that no VALU instruction waits on one
+    // issued just before it.
+    float ex[2][PER];
     auto stage_logit = [&](auto sc) __attribute__((always_inline)) {
       constexpr int sl = decltype(sc)::value;
 #pragma unroll
       for (int q = 0; q < PER; ++q) {
         const int e = sl * PER + q, bb = e >> 4, j = e & 15;
-        lg[sl & 1][q] = fmaf(cur[bb][j], a.c, -(PASS == 1 ? m2[bb] : lr[bb][j]));
+        cur[bb][j] = fmaf(cur[bb][j], a.c, -(PASS == 1 ? ref1[bb] : lr[bb][j]));
       }
     };
     auto stage_exp = [&](auto sc) __attribute__((always_inline)) {
       constexpr int sl = decltype(sc)::value;
 #pragma unroll
-      for (int q = 0; q < PER; ++q) ex[sl & 1][q] = fast_exp2(lg[sl & 1][q]);
+      for (int q = 0; q < PER; ++q) {
+        const int e = sl * PER + q, bb = e >> 4, j = e & 15;
+        ex[sl & 1][q] = fast_exp2(cur[bb][j]);
+      }
     };
     auto stage_sum = [&](auto sc) __attribute__((always_inline)) {
       constexpr int sl = decltype(sc)::value;
@@ -441,26 +451,38 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     stage_exp(std::integral_constant<int, NSL - 1>{});
     stage_sum(std::integral_constant<int, NSL - 2>{});
     stage_sum(std::integral_constant<int, NSL - 1>{});
+    // every partial sum is formed here, inside the MFMA sequence: without this
+    // the compiler sinks block 1's work past block 0's branch below
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) settle(p4[b][k]);
     if (PASS == 1) {
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
         const float sum = (p4[b][0] + p4[b][1]) + (p4[b][2] + p4[b][3]);
         const float nz = zs[b] + sum;
-        if (nz <= 0x1p64f) {  // keeps every later merge of (m2, zs) pairs finite
-          zs[b] = nz;
-        } else {  // too large (or not finite) under the current reference: move it to this tile's max
-          float tmax = cur[b][0];
+        // keeps every later merge of (m2, zs) pairs finite; otherwise (too large
+        // or not finite under the current reference) the reference moves to
+        // this tile's max. Wave-uniform branch, lane selects inside: the
+        // common path leaves the execution mask alone.
+        const bool big = !(nz <= 0x1p64f);
+        float znew = nz;
+        if (__builtin_amdgcn_ballot_w64(big) != 0) {
+          float tmax = cur[b][0];  // cur holds c*z - ref1 now
 #pragma unroll
           for (int j = 1; j < 16; ++j) tmax = fmaxf(tmax, cur[b][j]);
-          const float mnew = fmaxf(m2[b], tmax * a.c);
-          if (mnew != -INFINITY) {  // -inf: every key this lane has seen is hidden
-            float q4[4] = {0.f, 0.f, 0.f, 0.f};
+          const float mnew = fmaxf(m2[b], ref1[b] + tmax);
+          const float sh = mnew - ref1[b];
+          float q4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int j = 0; j < 16; ++j) q4[j & 3] += fast_exp2(fmaf(cur[b][j], a.c, -mnew));
-            zs[b] = fmaf(zs[b], fast_exp2(m2[b] - mnew), (q4[0] + q4[1]) + (q4[2] + q4[3]));
-            m2[b] = mnew;
-          }
+          for (int j = 0; j < 16; ++j) q4[j & 3] += fast_exp2(cur[b][j] - sh);
+          const float moved = fmaf(zs[b], fast_exp2(m2[b] - mnew), (q4[0] + q4[1]) + (q4[2] + q4[3]));
+          const bool mv = big && mnew != -INFINITY;  // -inf: every key this lane has seen is hidden
+          znew = mv ? moved : (big ? zs[b] : nz);
+          m2[b] = mv ? mnew : m2[b];
         }
+        zs[b] = znew;
         settle(zs[b]);  // keeps this iteration's VALU work inside this iteration
       }
     } else {
