@@ -17,10 +17,11 @@ using namespace stepkv;
 namespace {
 
 constexpr size_t kAlign = 256;
-#ifndef STEPKV_SAL_MIN_ITEMS
-#define STEPKV_SAL_MIN_ITEMS 2048
-#endif
-constexpr int kMinItems = STEPKV_SAL_MIN_ITEMS;  // saliency work items wanted: ~8 per CU on 256 CUs
+// Saliency work items: two resident workgroups on each of the 256 compute
+// units, and a workgroup start (its Q fragments and first K tiles) costs
+// about as long as six key tiles.
+constexpr int kSalSlots = 2 * 256;
+constexpr int kSalStartTiles = 6;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -74,13 +75,21 @@ SaliencyPlan plan_saliency(const stepkv_problem* pb) {
       t += (pb->cu_seqlens_host[s + 1] - pb->cu_seqlens_host[s] + c - 1) / c;
     return t;
   };
-  // largest chunk that still gives enough workgroups; all are multiples of
-  // every key tile (32, 64, 128)
-  p.chunk = 256;
-  for (int c : {16384, 8192, 4096, 2048, 1024, 512}) {
-    if (lh * chunks_for(c) >= kMinItems) {
+  // The chunk (a multiple of 128 keys, so every key tile divides it) with the
+  // least estimated makespan, rounds of resident workgroups times the tiles
+  // of one chunk plus a workgroup start; ties go to the longer chunk. Chunks
+  // stop at 4096 keys: with several rounds the two workgroups of a compute
+  // unit drift apart and each one's start hides under the other's sweep,
+  // which a single round of simultaneous starts does not allow.
+  const int tile = saliency_tile_keys(p.R);
+  p.chunk = 128;
+  int64_t best = -1;
+  for (int c = 128; c <= 4096; c += 128) {
+    const int64_t rounds = (lh * chunks_for(c) + kSalSlots - 1) / kSalSlots;
+    const int64_t cost = rounds * (c / tile + kSalStartTiles);
+    if (best < 0 || cost <= best) {
+      best = cost;
       p.chunk = c;
-      break;
     }
   }
   p.total_chunks = (int)chunks_for(p.chunk);

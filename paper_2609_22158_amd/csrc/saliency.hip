@@ -614,13 +614,23 @@ __global__ __launch_bounds__(kCombineThreads) void lse_combine_kernel(SaliencyAr
   const int ngrp = kCombineThreads / a.rows_pad;
   const int c0 = a.cu_chunks[s], c1 = a.cu_chunks[s + 1];
   const float2* __restrict__ pp = a.partial + (size_t)lh * a.total_chunks * a.rows_pad + row;
-  float M = -INFINITY;
-  for (int c = c0 + grp; c < c1; c += ngrp) M = fmaxf(M, pp[(size_t)c * a.rows_pad].x);
-  float Z = 0.f;
-  if (M != -INFINITY) {
-    for (int c = c0 + grp; c < c1; c += ngrp) {
-      const float2 p = pp[(size_t)c * a.rows_pad];
-      Z += p.y * exp2f(p.x - M);  // a chunk whose keys this row never saw: (-inf, 0) -> 0
+  // one online pass over this thread's chunks, eight loads in flight at a time;
+  // a chunk whose keys this row never saw is (-inf, 0) and adds nothing
+  float M = -INFINITY, Z = 0.f;
+  for (int c = c0 + grp; c < c1; c += 8 * ngrp) {
+    float2 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int cc = c + u * ngrp;
+      v[u] = cc < c1 ? pp[(size_t)cc * a.rows_pad] : make_float2(-INFINITY, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float Mn = fmaxf(M, v[u].x);
+      if (Mn != -INFINITY) {
+        Z = Z * exp2f(M - Mn) + v[u].y * exp2f(v[u].x - Mn);
+        M = Mn;
+      }
     }
   }
   part[threadIdx.x] = make_float2(M, Z);
