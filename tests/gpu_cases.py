@@ -40,7 +40,7 @@ def gpu_utilities(w) -> np.ndarray:
     return np.concatenate(out).astype(np.float32) if out else np.zeros(0, np.float32)
 
 
-class GpuRun:
+class HipRun:
     """Device copies of a workload and the HIP path's outputs."""
 
     def __init__(self, w, budget=None, params=None, want_v=True):

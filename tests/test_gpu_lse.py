@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 
 from paper_2609_22158_amd import binding as B
-from tests.gpu_cases import GpuRun, close, log, oracle_lse, reduced, run_oracle
+from tests.gpu_cases import HipRun, close, log, oracle_lse, reduced, run_oracle
 
 pytestmark = pytest.mark.gpu
 
@@ -54,7 +54,7 @@ def _compare(w, sc, o, what):
 @pytest.mark.parametrize("cid", list(CASES))
 def test_causal_two_sweeps_match_oracle(cid):
     w = _work(cid)
-    g = GpuRun(w, params=B.Params(causal_tail=1))
+    g = HipRun(w, params=B.Params(causal_tail=1))
     log(f"[causal {cid}] seqlens={w.seqlens} W={w.window} G={w.group}")
     sc = g.score(want_saliency=True)
     o = run_oracle(w, g.budget, g.params)
@@ -70,7 +70,7 @@ def test_causal_two_sweeps_match_oracle(cid):
 @pytest.mark.parametrize("cid", list(CASES))
 def test_window_lse_matches_oracle(cid, causal):
     w = _work(cid)
-    g = GpuRun(w, params=B.Params(causal_tail=causal), want_v=False)
+    g = HipRun(w, params=B.Params(causal_tail=causal), want_v=False)
     log(f"[window_lse {cid} causal={causal}]")
     got = B.window_lse(g.pb, g.q, g.k, g.params).cpu().numpy()
     want = oracle_lse(w, bool(causal))
@@ -85,7 +85,7 @@ def test_window_lse_matches_oracle(cid, causal):
 @pytest.mark.parametrize("cid", list(CASES))
 def test_lse_fed_single_sweep_matches_oracle(cid, causal):
     w = _work(cid)
-    g = GpuRun(w, params=B.Params(causal_tail=causal), want_v=False)
+    g = HipRun(w, params=B.Params(causal_tail=causal), want_v=False)
     lse32 = oracle_lse(w, bool(causal)).astype(np.float32)  # what a prefill would hand over
     log(f"[lse-fed {cid} causal={causal}]")
     sc = g.score(lse=g.lse_tensor(lse32), want_saliency=True)
@@ -96,7 +96,7 @@ def test_lse_fed_single_sweep_matches_oracle(cid, causal):
 def test_lse_fed_with_gpu_lse_equals_two_sweeps():
     """stepkv_window_lse followed by stepkv_saliency_from_lse reproduces stepkv_saliency."""
     w = _work("l1_tail3001")
-    g = GpuRun(w, want_v=False)
+    g = HipRun(w, want_v=False)
     lse = B.window_lse(g.pb, g.q, g.k, g.params)
     a1 = B.saliency_from_lse(g.pb, g.q, g.k, lse, g.params).cpu().numpy()
     a2 = B.saliency(g.pb, g.q, g.k, g.params).cpu().numpy()
@@ -107,7 +107,7 @@ def test_lse_fed_with_gpu_lse_equals_two_sweeps():
 def test_lse_shift_scales_rows():
     """Raising every row's LSE by ln 2 halves every saliency (a property at any size)."""
     w = _work("tiny")
-    g = GpuRun(w, want_v=False)
+    g = HipRun(w, want_v=False)
     lse = B.window_lse(g.pb, g.q, g.k, g.params)
     a1 = B.saliency_from_lse(g.pb, g.q, g.k, lse, g.params).cpu().numpy()
     a2 = B.saliency_from_lse(g.pb, g.q, g.k, lse + float(np.log(2.0)), g.params).cpu().numpy()

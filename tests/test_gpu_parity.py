@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 
 import oracle as O
-from tests.gpu_cases import (GpuRun, close, log, oracle_params, reduced, run_oracle, swap_ok)
+from tests.gpu_cases import (HipRun, close, log, oracle_params, reduced, run_oracle, swap_ok)
 
 pytestmark = pytest.mark.gpu
 
@@ -33,7 +33,7 @@ def _case(cid):
         name = spec.pop("name")
         log(f"[case {cid}] generating")
         w = reduced(name, **spec)
-        g = GpuRun(w)
+        g = HipRun(w)
         log(f"[case {cid}] gpu score, L={w.num_layers} seqlens={w.seqlens} W={w.window} "
             f"G={w.group} d={w.head_dim}")
         sc = g.score(want_saliency=True, want_stats=True)
@@ -84,7 +84,7 @@ def test_saliency_with_logit_spikes_matches_oracle():
             k[0, h, key] = f32_to_bf16_bits(factor * q[0, 0, wr, h * G + g])
             plants.append((h, key, wr * G + g, factor))
     w.k = k
-    g = GpuRun(w)
+    g = HipRun(w)
     sc = g.score(want_saliency=True)
     import torch
 
@@ -184,7 +184,7 @@ def test_budget_edges(budget):
     import torch
 
     w = reduced("tiny")
-    g = GpuRun(w, budget=budget)
+    g = HipRun(w, budget=budget)
     log(f"[budget {budget}] gpu")
     sc = g.score()
     idx, cu_ret, kept = g.select(sc["scores"], want_kept=True)
@@ -208,7 +208,7 @@ def test_single_signal_special_cases(alpha, beta):
 
     w = reduced("l1_8k", seqlens=[2049])
     p = B.Params(alpha=alpha, beta=beta)
-    g = GpuRun(w, params=p)
+    g = HipRun(w, params=p)
     log(f"[alpha {alpha} beta {beta}] gpu")
     sc = g.score()
     idx, _, _ = g.select(sc["scores"])
@@ -233,7 +233,7 @@ def test_token_only_selectors(selector):
 
     w = reduced("l1_8k", seqlens=[3001, 700], window=1 if selector == "last_query_only" else 32)
     p = getattr(B.Params, selector)()
-    g = GpuRun(w, params=p)
+    g = HipRun(w, params=p)
     log(f"[{selector}] W={w.window} pool={p.pool_kernel}")
     sc = g.score(want_saliency=True)
     o = run_oracle(w, g.budget, p)
@@ -252,7 +252,7 @@ def test_repeat_runs_are_bitwise_identical():
     import torch
 
     w = reduced("ragged16", num_layers=2, seqlens=[5003, 2100], num_steps=20)
-    g = GpuRun(w)
+    g = HipRun(w)
     rows = w.retained_rows(g.budget)
     outs = []
     for rep in range(3):
@@ -283,7 +283,7 @@ def test_decode_over_compacted_cache():
     from paper_2609_22158_amd import binding as B
 
     w = reduced("ragged16", num_layers=2, seqlens=[2500, 700, 130, 1, 4097], protected_len=64)
-    g = GpuRun(w)
+    g = HipRun(w)
     o = run_oracle(w, g.budget, g.params, want_saliency=False)
     P32, Pdev = _oracle_scores_fp32(w, o)
     idx, cu_ret, _ = g.select(Pdev)
@@ -313,7 +313,7 @@ def test_full_size_bench_configuration_sampled():
     from synth import make_workload
 
     w = make_workload("l32_32k", 233)
-    g = GpuRun(w)
+    g = HipRun(w)
     log("[full l32_32k] gpu pass")
     sc = g.score(want_saliency=True)
     idx, cu, _ = g.select(sc["scores"])

@@ -10,7 +10,7 @@ import pytest
 
 import oracle as O
 from paper_2609_22158_amd import binding as B
-from tests.gpu_cases import (GpuRun, close, log, oracle_lse, oracle_params, oracle_utilities,
+from tests.gpu_cases import (HipRun, close, log, oracle_lse, oracle_params, oracle_utilities,
                              reduced, swap_ok)
 
 pytestmark = pytest.mark.gpu
@@ -30,7 +30,7 @@ def _case(cid):
     if cid not in _c:
         spec = dict(CASES[cid])
         w = reduced(spec.pop("name"), **spec)
-        g = GpuRun(w)
+        g = HipRun(w)
         log(f"[shared {cid}] L={w.num_layers} seqlens={w.seqlens} W={w.window} G={w.group}")
         sc = B.score_shared(g.pb, g.q, g.k, g.sid, g.prot, g.util, g.params, last_layers=LAST,
                             want_saliency=True)
