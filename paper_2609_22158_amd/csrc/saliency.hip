@@ -64,9 +64,10 @@ __device__ __forceinline__ void wait_tiles(int ahead) {
 #define STEPKV_SAL_RING_BYTES (TILE_BYTES <= 8192 ? 32768 : 65536)
 #endif
 
-// Make the compiler wait for the load that produced x here, once, instead of
-// at the first use inside the tile loop, where its wait would also drain the
-// K prefetch ring on every iteration.
+// Pins x to this point of the program: the compiler must have x here (it
+// waits for the load that produced it here, once, instead of at a first use
+// inside the tile loop, where the wait would also drain the K prefetch ring),
+// and cannot sink the computation of x past this point.
 template <typename T>
 __device__ __forceinline__ void settle(T& x) {
   asm volatile("" : "+v"(x));
