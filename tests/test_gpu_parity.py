@@ -348,3 +348,73 @@ def test_full_size_bench_configuration_sampled():
         kh = k2[l, h].view(torch.int16).cpu().numpy().view(np.uint16)
         vh = v2[l, h].view(torch.int16).cpu().numpy().view(np.uint16)
         assert np.array_equal(kh, w.k[l, h][want]) and np.array_equal(vh, w.v[l, h][want])
+
+
+def test_full_size_lse_fed_configuration_sampled():
+    """The bench's --lse-fed configuration at full size (32 layers, 32k tokens, W=64):
+    the row LSEs come from stepkv_window_lse, as in the bench, and feed the one-sweep
+    scoring. Every head is checked by its saliency mass, sampled heads against the
+    oracle's exact softmax saliency and priorities one by one."""
+    import torch
+
+    from paper_2609_22158_amd import binding as B
+    from synth import make_workload
+
+    w = make_workload("l32_32k", 233)
+    g = HipRun(w)
+    log("[full l32_32k lse-fed] gpu window LSE and one sweep")
+    ws = torch.empty(g.pb.saliency_workspace_bytes(), dtype=torch.uint8, device="cuda")
+    lse = B.window_lse(g.pb, g.q, g.k, g.params, workspace=ws)
+    sc = g.score(lse=lse, want_saliency=True)
+    torch.cuda.synchronize()
+    R = w.window * w.group
+    A = sc["saliency"].cpu().numpy()
+    np.testing.assert_allclose(A.sum(axis=2), R, rtol=1e-4)
+    heads = [(0, 3), (17, 0), (31, 6)]
+    log("[full l32_32k lse-fed] oracle on sampled heads")
+    o = run_oracle(w, g.budget, g.params, heads=heads)
+    P = sc["scores"].cpu().numpy()
+    for l, h in heads:
+        close(A[l, h], o["A"][(0, l, h)], f"A{(l, h)} lse-fed")
+        close(P[l, h], o["P"][(0, l, h)], f"P{(l, h)} lse-fed")
+
+
+def test_full_size_shared_configuration():
+    """The bench's --shared-layers 3 configuration at full size: the summed saliency of
+    the last 3 layers (24 KV heads x 32k tokens), the single priority row, its ranking
+    and the gather of all 32 layers x 8 heads, against the oracle's compress_shared."""
+    import torch
+
+    from paper_2609_22158_amd import binding as B
+    from synth import make_workload
+    from tests.gpu_cases import oracle_utilities
+
+    w = make_workload("l32_32k", 233)
+    g = HipRun(w)
+    log("[full l32_32k shared] gpu pass")
+    sc = B.score_shared(g.pb, g.q, g.k, g.sid, g.prot, g.util, g.params, last_layers=3,
+                        want_saliency=True)
+    torch.cuda.synchronize()
+    log("[full l32_32k shared] oracle")
+    o = O.compress_shared(w.q_win, w.k, None, w.cu_seqlens, w.step_ids, w.protected, w.cu_steps,
+                          oracle_utilities(w), g.budget, oracle_params(g.params), last_layers=3,
+                          want_kv=False)
+    A = sc["saliency"].cpu().numpy()
+    P = sc["scores"].cpu().numpy()
+    close(A, o["A"][0], "A shared full")
+    close(P, o["P"][0], "P shared full")
+    mass = 3 * w.num_kv_heads * w.window * w.group
+    assert abs(A.sum() - mass) < 1e-3 * mass
+    # selection on the oracle's priorities (fp32) and the gather of every layer and head
+    P32 = o["P"][0].astype(np.float32)
+    sel = B.select_shared(g.pb, torch.from_numpy(P32).cuda(), g.prot, g.sid, g.budget)
+    idx, cu = sel["idx"], sel["cu_retained"]
+    rows = w.retained_rows(g.budget)[0]
+    k_hat, v_hat = B.compact_shared(g.pb, g.k, g.v, idx, cu, rows)
+    torch.cuda.synchronize()
+    want = O.select_retained(P32, w.protected == 0, g.budget)
+    got = idx.cpu().numpy()[:rows]
+    assert np.array_equal(got, want)
+    kh = k_hat.view(torch.int16).cpu().numpy().view(np.uint16)
+    for l, h in [(0, 0), (16, 4), (31, 7)]:
+        assert np.array_equal(kh[l, h], w.k[l, h][want]), (l, h)
