@@ -15,6 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libstepkv.so")
+C_DEMO_SRC = os.path.join(ROOT, "tests", "c_abi", "compress_demo.c")
+C_DEMO = os.path.join(ROOT, "tests", "c_abi", "compress_demo")
 
 SOURCES = ["api.cpp", "step_text.cpp", "saliency.hip", "fuse.hip", "select.hip", "compact.hip",
            "decode.hip"]
@@ -68,7 +70,19 @@ def build(verbose: bool = False, extra_flags=(), lib_path: str = LIB) -> str:
     tmp = lib_path + ".tmp"
     _run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Wl,-z,defs", "-o", tmp, *objs])
     os.replace(tmp, lib_path)
+    if lib_path == LIB and os.path.exists(C_DEMO_SRC):
+        build_c_demo()
     return lib_path
+
+
+def build_c_demo() -> str:
+    """Compile the plain-C consumer of the ABI (tests/c_abi) against the in-tree library."""
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(_hipcc())))
+    _run(["gcc", "-std=c11", "-O2", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__",
+          f"-I{rocm}/include", f"-I{INCLUDE}", C_DEMO_SRC, "-o", C_DEMO, f"-L{PKG}", "-lstepkv",
+          f"-L{rocm}/lib", "-lamdhip64", "-lm", "-Wl,-rpath,$ORIGIN/../../paper_2609_22158_amd",
+          f"-Wl,-rpath,{rocm}/lib"])
+    return C_DEMO
 
 
 if __name__ == "__main__":
