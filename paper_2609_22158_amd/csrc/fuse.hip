@@ -332,13 +332,22 @@ namespace {
 
 // Shared-index mode: A_i = sum of the window saliency of `heads` (layer, KV
 // head) rows, added in row order (deterministic). Coalesced: consecutive
-// threads read consecutive tokens of each row.
+// threads read consecutive tokens of each row; eight rows' loads are in
+// flight before their adds.
 __global__ __launch_bounds__(256) void sum_heads_kernel(const float* __restrict__ sal, int heads,
                                                         int ntot, float* __restrict__ out) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= ntot) return;
   float acc = sal[i];
-  for (int h = 1; h < heads; ++h) acc += sal[(size_t)h * ntot + i];
+  int h = 1;
+  for (; h + 8 <= heads; h += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = sal[(size_t)(h + u) * ntot + i];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += v[u];
+  }
+  for (; h < heads; ++h) acc += sal[(size_t)h * ntot + i];
   out[i] = acc;
 }
 
