@@ -214,6 +214,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
       prot_bits |= pr << j;
       npr += keys[j] != 0u ? 1 : 0;
     }
+    asm volatile("" : "+v"(prot_bits));  // rebuilt from lane masks otherwise
   } else {
     for (int j = 0; j < nslots; ++j) npr += (tid + kThreads * j < ns && prot[tid + kThreads * j] == 0);
   }
@@ -262,6 +263,12 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
       uint32_t prefix = kmax & pmask;
       int krem = ktake;
       while (lo > 0) {
+        // fresh compares in every pass: otherwise the compiler keeps 32 lane
+        // masks of `key != 0` alive across the passes and spills them
+        if (CACHED) {
+#pragma unroll
+          for (int j = 0; j < kCached; ++j) asm volatile("" : "+v"(keys[j]));
+        }
         const int width = min(kDigitBits, lo);
         const int shift = lo - width;
         const int nbins = 1 << width;
@@ -273,8 +280,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
         };
         if (CACHED) {
 #pragma unroll
-          for (int j = 0; j < kCached; ++j)
-            if (kThreads * j < ns) count(keys[j]);
+          for (int j = 0; j < kCached; ++j) count(keys[j]);  // slots past N hold key 0: no candidate
         } else {
           for (int j = 0; j < nslots; ++j) count(key_at(j));
         }
@@ -324,6 +330,10 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
     }
   }
 
+  if (CACHED) {
+#pragma unroll
+    for (int j = 0; j < kCached; ++j) asm volatile("" : "+v"(keys[j]));
+  }
   // ---- ordered write-out
   int32_t* __restrict__ out = a.idx + (size_t)lh * a.ntot + seq0;
   const int32_t* __restrict__ sid = a.step_ids + seq0;
