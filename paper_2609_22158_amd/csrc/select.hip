@@ -11,6 +11,12 @@
 // positions first), protected tokens are always kept. Histogram increments are
 // aggregated per wave with ballots (scores cluster by step utility, so most
 // lanes of a wave share a digit) before the LDS atomics.
+//
+// Sequences of up to 32768 tokens keep their keys in registers (32 per
+// thread, position tid + 1024 j in slot j); longer ones re-read the scores
+// in every pass. The work per key is plain VALU arithmetic over lane data;
+// per-slot lane masks are made where they are used, never held across a
+// phase, since 32 of them do not fit the scalar registers.
 #include "common.h"
 #include "internal.h"
 
@@ -27,6 +33,13 @@ __device__ __forceinline__ uint32_t order_key(float p) {
   u = u == 0x80000000u ? 0u : u;                           // -0 ranks as +0
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);       // never 0 for canonical values
 }
+
+// In registers, a protected token holds this key: above every score's key
+// (+inf maps to 0xFF800000), so it is kept by the same test as a score above
+// tau; positions past the sequence hold 0. Neither is a candidate.
+constexpr uint32_t kProtKey = 0xFFFFFFFFu;
+// No score maps to key 1 (it would be a NaN's), so `key == 1` is never a tie.
+constexpr uint32_t kNoKey = 1u;
 
 constexpr int kDigitBits = 11;
 constexpr int kBins = 1 << kDigitBits;
@@ -57,71 +70,155 @@ __device__ __forceinline__ int block_sum_int(int v, int* scratch) {
   return t;
 }
 
-// Exclusive prefix sum over the workgroup in thread order; `total` gets the sum.
-__device__ __forceinline__ int block_exclusive_scan(int v, int* scratch, int& total) {
+// Exclusive prefix sum over the workgroup in thread order (modulo 2^32).
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* scratch) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int inc = v;
+  uint32_t inc = v;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    const int x = __shfl_up(inc, o, kWave);
+    const uint32_t x = (uint32_t)__shfl_up((int)inc, o, kWave);
     if (lane >= o) inc += x;
   }
   if (lane == 63) scratch[wave] = inc;
   __syncthreads();
-  int before = 0, tot = 0;
-  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
-    const int c = scratch[w];
-    before += w < wave ? c : 0;
-    tot += c;
-  }
+  uint32_t before = 0u;
+  for (int w = 0; w < wave; ++w) before += scratch[w];
   __syncthreads();
-  total = tot;
   return before + inc - v;
 }
 
-// Exclusive prefix sums of four counters at once over the workgroup in
-// thread order; `total` gets the four sums. scratch holds 4 * waves ints.
-__device__ __forceinline__ int4 block_exclusive_scan4(int4 v, int* scratch, int4& total) {
+// Kept candidates of one slot grouped by step: one atomic per step per wave.
+__device__ __forceinline__ void count_kept_steps(int32_t* kept, int nsteps, int k, int lane) {
+  const bool ok = k >= 0 && k < nsteps;
+  uint64_t pend = ballot(ok);
+  while (pend) {
+    const int leader = __builtin_ctzll(pend);
+    const int kk = __shfl(k, leader, kWave);
+    const uint64_t grp = ballot(ok && k == kk);
+    if (lane == leader) atomicAdd(&kept[kk], (int)__popcll(grp));
+    pend &= ~grp;
+  }
+}
+
+// Candidate count and key range over the workgroup in one barrier round.
+// hist[0..kBins) is cleared before the same barrier for the first pass.
+__device__ __forceinline__ void reduce_count_range(int& npr, uint32_t& kmin, uint32_t& kmax,
+                                                   uint32_t (*red)[kWaves], uint32_t* hist) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nw = (int)(blockDim.x >> 6);
-  int4 inc = v;
+  for (int e = threadIdx.x; e < kBins; e += kThreads) hist[e] = 0u;
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int4 x = make_int4(__shfl_up(inc.x, o, kWave), __shfl_up(inc.y, o, kWave),
-                             __shfl_up(inc.z, o, kWave), __shfl_up(inc.w, o, kWave));
-    if (lane >= o) {
-      inc.x += x.x;
-      inc.y += x.y;
-      inc.z += x.z;
-      inc.w += x.w;
-    }
+  for (int o = 32; o > 0; o >>= 1) {
+    kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o, kWave));
+    kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o, kWave));
   }
-  if (lane == 63) {
-    scratch[4 * wave] = inc.x;
-    scratch[4 * wave + 1] = inc.y;
-    scratch[4 * wave + 2] = inc.z;
-    scratch[4 * wave + 3] = inc.w;
+  if (lane == 0) {
+    red[0][wave] = (uint32_t)npr;
+    red[1][wave] = kmin;
+    red[2][wave] = kmax;
   }
   __syncthreads();
-  int4 before = make_int4(0, 0, 0, 0), tot = make_int4(0, 0, 0, 0);
-  for (int w = 0; w < nw; ++w) {
-    const int4 c = make_int4(scratch[4 * w], scratch[4 * w + 1], scratch[4 * w + 2],
-                             scratch[4 * w + 3]);
-    if (w < wave) {
-      before.x += c.x;
-      before.y += c.y;
-      before.z += c.z;
-      before.w += c.w;
-    }
-    tot.x += c.x;
-    tot.y += c.y;
-    tot.z += c.z;
-    tot.w += c.w;
+  npr = 0;
+  for (int w = 0; w < kWaves; ++w) {
+    npr += (int)red[0][w];
+    kmin = min(kmin, red[1][w]);
+    kmax = max(kmax, red[2][w]);
   }
-  __syncthreads();
-  total = tot;
-  return make_int4(before.x + inc.x - v.x, before.y + inc.y - v.y, before.z + inc.z - v.z,
-                   before.w + inc.w - v.w);
+}
+
+// MSB-first radix search for the key tau of the ktake-th largest candidate
+// (kmin..kmax: candidate key range, kmin < kmax) and the number `need` of
+// tokens equal to tau that are kept. count(h, pmask, prefix, shift, nbins)
+// adds each candidate key with (key & pmask) == prefix to bin
+// (key >> shift) & (nbins - 1) of h. Two histograms alternate: each pass
+// counts into one and clears the other, which only the previous pass read;
+// the first must be clear and visible on entry.
+template <typename Count>
+__device__ __forceinline__ void radix_search(uint32_t kmin, uint32_t kmax, int ktake,
+                                             uint32_t* hist, int* sh, Count count, uint32_t& tau,
+                                             int& need) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int lo = 32 - __builtin_clz(kmin ^ kmax);  // undecided low bits
+  const uint32_t low = lo == 32 ? 0xFFFFFFFFu : ((1u << lo) - 1u);
+  uint32_t pmask = ~low;
+  uint32_t prefix = kmax & pmask;
+  int krem = ktake;
+  int buf = 0;
+  while (lo > 0) {
+    const int width = min(kDigitBits, lo);
+    const int shift = lo - width;
+    const int nbins = 1 << width;
+    uint32_t* h = hist + buf * kBins;
+    uint32_t* hn = hist + (buf ^ 1) * kBins;
+    for (int e = tid; e < kBins; e += kThreads) hn[e] = 0u;
+    count(h, pmask, prefix, shift, nbins);
+    __syncthreads();
+    if (wave == 0) {
+      // lane owns bins 32*lane .. 32*lane+31 (bins >= nbins stay zero);
+      // find the bin holding the krem-th largest key
+      constexpr int kPer = kBins / kWave;
+      int b0 = kPer * lane;
+      asm volatile("" : "+v"(b0));  // bin numbers made here, not held across passes
+      const uint4* hp = reinterpret_cast<const uint4*>(h + b0);
+      uint32_t own = 0u;
+#pragma unroll
+      for (int q = 0; q < kPer / 4; ++q) {
+        const uint4 h4 = hp[q];
+        own += (h4.x + h4.y) + (h4.z + h4.w);
+      }
+      uint32_t suf = own;  // inclusive suffix over lanes >= lane
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t x = __shfl_down(suf, o, kWave);
+        if (lane + o < 64) suf += x;
+      }
+      uint32_t above = suf - own;  // keys in bins owned by higher lanes
+      auto visit = [&](uint32_t c, int bin) {
+        if (above < (uint32_t)krem && (uint32_t)krem <= above + c) {
+          sh[0] = bin;
+          sh[1] = krem - (int)above;
+        }
+        above += c;
+      };
+#pragma unroll
+      for (int q = kPer / 4 - 1; q >= 0; --q) {  // bins from high to low
+        const uint4 h4 = hp[q];
+        visit(h4.w, b0 + 4 * q + 3);
+        visit(h4.z, b0 + 4 * q + 2);
+        visit(h4.y, b0 + 4 * q + 1);
+        visit(h4.x, b0 + 4 * q);
+      }
+    }
+    __syncthreads();
+    prefix |= (uint32_t)sh[0] << shift;
+    pmask |= (uint32_t)(nbins - 1) << shift;
+    krem = sh[1];
+    lo = shift;
+    buf ^= 1;
+  }
+  tau = prefix;
+  need = krem;  // tokens equal to tau that are kept, lowest positions first
+}
+
+struct RowSetup {
+  int s, lh, seq0, ns, B, nsteps;
+  int32_t* kept;
+};
+
+__device__ __forceinline__ RowSetup row_setup(const SelectArgs& a) {
+  RowSetup r;
+  r.s = blockIdx.x / a.LH;
+  r.lh = blockIdx.x - r.s * a.LH;
+  r.seq0 = a.cu_seqlens[r.s];
+  r.ns = a.cu_seqlens[r.s + 1] - r.seq0;
+  r.B = a.budgets ? max(1, a.budgets[r.s]) : a.budget;
+  const int st0 = a.kept ? a.cu_steps[r.s] : 0;
+  r.nsteps = a.kept ? a.cu_steps[r.s + 1] - st0 : 0;
+  r.kept = a.kept ? a.kept + (size_t)r.lh * a.total_steps + st0 : nullptr;
+  if (r.kept) {
+    for (int k = threadIdx.x; k < r.nsteps; k += kThreads) r.kept[k] = 0;
+    __threadfence();  // the zeros reach L2 before any wave's atomics below
+  }
+  return r;
 }
 
 // cu_retained[s+1] - cu_retained[s] = n_protected_s + min(B_s, N_s - n_protected_s)
@@ -158,30 +255,143 @@ __global__ __launch_bounds__(kThreads) void retained_plan_kernel(SelectArgs a) {
   }
 }
 
-template <bool CACHED>
-__global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
-  __shared__ __attribute__((aligned(16))) uint32_t hist[3 * kThreads];  // histogram, then bitmasks
-  __shared__ int scratch[4 * kWaves];
-  __shared__ uint32_t kred[2][kWaves];
-  __shared__ int wcnt[2][2][kWaves];
-  __shared__ int sh_digit, sh_krem;
+// ---------------------------------------------------------------- N_s <= 32768
+__global__ __launch_bounds__(kThreads) void select_cached_kernel(SelectArgs a) {
+  __shared__ __attribute__((aligned(16))) uint32_t hist[2 * kBins];
+  __shared__ uint32_t red[3][kWaves];
+  __shared__ int sh[2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int s = blockIdx.x / a.LH, lh = blockIdx.x - s * a.LH;
-  const int seq0 = a.cu_seqlens[s];
-  const int ns = a.cu_seqlens[s + 1] - seq0;
-  const float* __restrict__ P = a.scores + (size_t)lh * a.ntot + seq0;
-  const uint8_t* __restrict__ prot = a.prot + seq0;
-  const int B = a.budgets ? max(1, a.budgets[s]) : a.budget;
-  const int st0 = a.kept ? a.cu_steps[s] : 0;
-  const int nsteps = a.kept ? a.cu_steps[s + 1] - st0 : 0;
-  int32_t* kept = a.kept ? a.kept + (size_t)lh * a.total_steps + st0 : nullptr;
-  if (kept) {
-    for (int k = tid; k < nsteps; k += kThreads) kept[k] = 0;
-    __threadfence();  // the zeros reach L2 before any wave's atomics below
+  const RowSetup r = row_setup(a);
+  const int ns = r.ns;
+  const float* __restrict__ P = a.scores + (size_t)r.lh * a.ntot + r.seq0;
+  const uint8_t* __restrict__ prot = a.prot + r.seq0;
+
+  // every load issued before any is used: indices clamped into the sequence
+  float pv[kCached];
+  uint32_t pb[kCached];
+  if (ns > 0) {
+#pragma unroll
+    for (int j = 0; j < kCached; ++j) {
+      const int ic = min(tid + kThreads * j, ns - 1);
+      pv[j] = P[ic];
+      pb[j] = prot[ic];
+    }
+  }
+  uint32_t keys[kCached];
+  int npr = 0;  // wave total
+  uint32_t kmin1 = 0xFFFFFFFFu, kmax1 = 0u;  // candidate key - 1 and + 1
+#pragma unroll
+  for (int j = 0; j < kCached; ++j) {
+    // NaN -> -inf and -0 -> +0 in float arithmetic, then the sign flip
+    const float q = fmaxf(pv[j], -INFINITY) + 0.0f;
+    const uint32_t u = __float_as_uint(q);
+    const uint32_t key = u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+    const bool in = tid + kThreads * j < ns;
+    keys[j] = in ? (pb[j] == 0u ? key : kProtKey) : 0u;
+    // key - 1 wraps 0 to the top and puts kProtKey just below it
+    const uint32_t km = keys[j] - 1u;
+    npr += __popcll(ballot(km < kProtKey - 1u));
+    kmin1 = min(kmin1, km);
+    kmax1 = max(kmax1, keys[j] + 1u);  // kProtKey + 1 wraps to 0
+  }
+  // reduced in the shifted domains, where non-candidates lose every min and max
+  reduce_count_range(npr, kmin1, kmax1, red, hist);
+  const uint32_t kmin = kmin1 + 1u, kmax = kmax1 - 1u;  // used only when there are candidates
+  const int ktake = min(r.B, npr);
+  const bool take_all = ktake == npr;
+
+  uint32_t tau = 0u;
+  int need = 0;
+  if (!take_all) {
+    if (kmin == kmax) {
+      tau = kmin;  // every candidate ties
+      need = ktake;
+    } else {
+      auto count = [&](uint32_t* h, uint32_t pmask, uint32_t prefix, int shift, int nbins) {
+        // fresh compares in every pass rather than lane masks held across passes
+#pragma unroll
+        for (int j = 0; j < kCached; ++j) asm volatile("" : "+v"(keys[j]));
+        const uint32_t dm = (uint32_t)(nbins - 1);
+        if (prefix != 0u && prefix != pmask) {
+          // neither 0 nor kProtKey can match the prefix
+#pragma unroll
+          for (int j = 0; j < kCached; ++j)
+            wave_hist_add(h, (keys[j] & pmask) == prefix, (keys[j] >> shift) & dm, lane);
+        } else {
+#pragma unroll
+          for (int j = 0; j < kCached; ++j)
+            wave_hist_add(h, (keys[j] & pmask) == prefix && keys[j] - 1u < kProtKey - 1u,
+                          (keys[j] >> shift) & dm, lane);
+        }
+      };
+      radix_search(kmin, kmax, ktake, hist, sh, count, tau, need);
+    }
   }
 
+  // ---- ordered write-out. Ranks in position order straight from the
+  // strided slots: per (slot, wave) the numbers of sure keeps and of ties,
+  // one exclusive scan over the 512 (slot, wave) pairs, which are already in
+  // position order, and ballots for the ranks inside a wave. A tie is kept
+  // when fewer than `need` ties precede it, so the tokens kept before
+  // position p are the sure keeps before p plus min(ties before p, need).
+  int32_t* __restrict__ out = a.idx + (size_t)r.lh * a.ntot + r.seq0;
+  const uint32_t t_sure = take_all ? 0u : tau;    // key > t_sure: kept for sure
+  const uint32_t t_tie = take_all ? kNoKey : tau;  // key == t_tie: a tie
+  uint32_t* cnt = hist;  // [kCached][kWaves]: sure | ties << 16
+#pragma unroll
+  for (int j = 0; j < kCached; ++j) asm volatile("" : "+v"(keys[j]));
+#pragma unroll
+  for (int j = 0; j < kCached; ++j) {
+    const uint32_t c = (uint32_t)__popcll(ballot(keys[j] > t_sure)) |
+                       ((uint32_t)__popcll(ballot(keys[j] == t_tie)) << 16);
+    if (lane == 0) cnt[j * kWaves + wave] = c;
+  }
+  __syncthreads();
+  // at most 32768 tokens: both halves of the packed sums stay below 2^16
+  const uint32_t ex = block_exclusive_scan(tid < kCached * kWaves ? cnt[tid] : 0u, red[0]);
+  if (tid < kCached * kWaves) cnt[tid] = ex;
+  __syncthreads();
+  const uint32_t base_lane = lane < kCached ? cnt[lane * kWaves + wave] : 0u;
+#pragma unroll
+  for (int j = 0; j < kCached; ++j) asm volatile("" : "+v"(keys[j]));
+  const int32_t* __restrict__ sid = a.step_ids + r.seq0;
+  int tid_w = tid;
+  asm volatile("" : "+v"(tid_w));  // positions and addresses made here, not carried from the top
+#pragma unroll
+  for (int j = 0; j < kCached; ++j) {
+    const bool sure = keys[j] > t_sure, tie = keys[j] == t_tie;
+    const uint64_t bs = ballot(sure), bt = ballot(tie);
+    if ((bs | bt) == 0ull) continue;
+    const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)base_lane, j);
+    const int s_before = (int)(base & 0xFFFFu) + lanes_below(bs);
+    const int t_before = (int)(base >> 16) + lanes_below(bt);
+    const bool keep = sure || (tie && t_before < need);
+    const int i = tid_w + kThreads * j;
+    if (keep) out[s_before + min(t_before, need)] = i;
+    if (r.kept) {
+      const bool cand = keys[j] - 1u < kProtKey - 1u;
+      count_kept_steps(r.kept, r.nsteps, (keep && cand) ? sid[i] : -1, lane);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- N_s > 32768
+// Keys are re-read from the scores in every pass; the write-out ranks one
+// slot at a time with two barrier rounds per slot.
+__global__ __launch_bounds__(kThreads) void select_stream_kernel(SelectArgs a) {
+  __shared__ __attribute__((aligned(16))) uint32_t hist[2 * kBins];
+  __shared__ uint32_t red[3][kWaves];
+  __shared__ int wcnt[2][2][kWaves];
+  __shared__ int sh[2];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const RowSetup r = row_setup(a);
+  const int ns = r.ns;
+  const float* __restrict__ P = a.scores + (size_t)r.lh * a.ntot + r.seq0;
+  const uint8_t* __restrict__ prot = a.prot + r.seq0;
   // position of slot j of this thread: tid + kThreads * j (coalesced)
   auto key_at = [&](int j) -> uint32_t {
     const int i = tid + kThreads * j;
@@ -189,248 +399,42 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
     return order_key(P[i]);
   };
   const int nslots = (ns + kThreads - 1) / kThreads;
-  uint32_t keys[CACHED ? kCached : 1];
-  uint32_t prot_bits = 0;  // bit j: position tid + 1024 j is protected
   int npr = 0;
-  if (CACHED) {
-    // every load issued before any is used: indices clamped into the sequence
-    float pv[kCached];
-    uint32_t pb[kCached];
-    if (ns > 0) {
-#pragma unroll
-      for (int j = 0; j < kCached; ++j) {
-        const int ic = min(tid + kThreads * j, ns - 1);
-        pv[j] = P[ic];
-        pb[j] = prot[ic];
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < kCached; ++j) {
-      // branch-free: selects only, so no per-slot lane masks stay live
-      const uint32_t in = (uint32_t)(tid + kThreads * j - ns) >> 31;  // 1 if inside
-      const uint32_t pr = in & (pb[j] != 0u ? 1u : 0u);
-      const uint32_t key = order_key(pv[j]);
-      keys[j] = (in & (pr ^ 1u)) ? key : 0u;
-      prot_bits |= pr << j;
-      npr += keys[j] != 0u ? 1 : 0;
-    }
-    asm volatile("" : "+v"(prot_bits));  // rebuilt from lane masks otherwise
-  } else {
-    for (int j = 0; j < nslots; ++j) npr += (tid + kThreads * j < ns && prot[tid + kThreads * j] == 0);
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+  for (int j = 0; j < nslots; ++j) {
+    const uint32_t key = key_at(j);
+    npr += key != 0u ? 1 : 0;
+    kmin = min(kmin, key != 0u ? key : 0xFFFFFFFFu);
+    kmax = max(kmax, key);
   }
-  npr = block_sum_int(npr, scratch);  // also orders the kept[] zeroing before its atomics
-  const int ktake = min(B, npr);
+  npr = wave_sum_int(npr);
+  reduce_count_range(npr, kmin, kmax, red, hist);
+  const int ktake = min(r.B, npr);
   const bool take_all = ktake == npr;
 
   uint32_t tau = 0u;
   int need = 0;
   if (!take_all) {
-    // range of the candidate keys: bits above the highest differing bit are shared
-    uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
-    auto range = [&](uint32_t key) {
-      if (key != 0u) {
-        kmin = min(kmin, key);
-        kmax = max(kmax, key);
-      }
-    };
-    if (CACHED) {
-#pragma unroll
-      for (int j = 0; j < kCached; ++j) range(keys[j]);
-    } else {
-      for (int j = 0; j < nslots; ++j) range(key_at(j));
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o, kWave));
-      kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o, kWave));
-    }
-    if (lane == 0) {
-      kred[0][wave] = kmin;
-      kred[1][wave] = kmax;
-    }
-    __syncthreads();
-    for (int w = 0; w < kWaves; ++w) {
-      kmin = min(kmin, kred[0][w]);
-      kmax = max(kmax, kred[1][w]);
-    }
     if (kmin == kmax) {
-      tau = kmin;  // every candidate ties
+      tau = kmin;
       need = ktake;
     } else {
-      int lo = 32 - __builtin_clz(kmin ^ kmax);  // undecided low bits
-      const uint32_t low = lo == 32 ? 0xFFFFFFFFu : ((1u << lo) - 1u);
-      uint32_t pmask = ~low;
-      uint32_t prefix = kmax & pmask;
-      int krem = ktake;
-      while (lo > 0) {
-        // fresh compares in every pass: otherwise the compiler keeps 32 lane
-        // masks of `key != 0` alive across the passes and spills them
-        if (CACHED) {
-#pragma unroll
-          for (int j = 0; j < kCached; ++j) asm volatile("" : "+v"(keys[j]));
+      auto count = [&](uint32_t* h, uint32_t pmask, uint32_t prefix, int shift, int nbins) {
+        for (int j = 0; j < nslots; ++j) {
+          const uint32_t key = key_at(j);
+          wave_hist_add(h, key != 0u && (key & pmask) == prefix,
+                        (key >> shift) & (uint32_t)(nbins - 1), lane);
         }
-        const int width = min(kDigitBits, lo);
-        const int shift = lo - width;
-        const int nbins = 1 << width;
-        for (int e = tid; e < kBins; e += kThreads) hist[e] = 0u;
-        __syncthreads();
-        auto count = [&](uint32_t key) {
-          const bool cand = key != 0u && (key & pmask) == prefix;
-          wave_hist_add(hist, cand, (key >> shift) & (uint32_t)(nbins - 1), lane);
-        };
-        if (CACHED) {
-#pragma unroll
-          for (int j = 0; j < kCached; ++j) count(keys[j]);  // slots past N hold key 0: no candidate
-        } else {
-          for (int j = 0; j < nslots; ++j) count(key_at(j));
-        }
-        __syncthreads();
-        if (wave == 0) {
-          // lane owns bins 32*lane .. 32*lane+31 (bins >= nbins stay zero);
-          // find the bin holding the krem-th largest key
-          constexpr int kPer = kBins / kWave;
-          const uint4* hp = reinterpret_cast<const uint4*>(hist + kPer * lane);
-          uint32_t own = 0u;
-#pragma unroll
-          for (int q = 0; q < kPer / 4; ++q) {
-            const uint4 h4 = hp[q];
-            own += (h4.x + h4.y) + (h4.z + h4.w);
-          }
-          uint32_t suf = own;  // inclusive suffix over lanes >= lane
-#pragma unroll
-          for (int o = 1; o < 64; o <<= 1) {
-            const uint32_t x = __shfl_down(suf, o, kWave);
-            if (lane + o < 64) suf += x;
-          }
-          uint32_t above = suf - own;  // keys in bins owned by higher lanes
-          auto visit = [&](uint32_t c, int bin) {
-            if (above < (uint32_t)krem && (uint32_t)krem <= above + c) {
-              sh_digit = bin;
-              sh_krem = krem - (int)above;
-            }
-            above += c;
-          };
-#pragma unroll
-          for (int q = kPer / 4 - 1; q >= 0; --q) {  // bins from high to low
-            const uint4 h4 = hp[q];
-            visit(h4.w, kPer * lane + 4 * q + 3);
-            visit(h4.z, kPer * lane + 4 * q + 2);
-            visit(h4.y, kPer * lane + 4 * q + 1);
-            visit(h4.x, kPer * lane + 4 * q);
-          }
-        }
-        __syncthreads();
-        prefix |= (uint32_t)sh_digit << shift;
-        pmask |= (uint32_t)(nbins - 1) << shift;
-        krem = sh_krem;
-        lo = shift;
-      }
-      tau = prefix;
-      need = krem;  // tokens equal to tau that are kept, lowest positions first
+      };
+      radix_search(kmin, kmax, ktake, hist, sh, count, tau, need);
     }
   }
 
-  if (CACHED) {
-#pragma unroll
-    for (int j = 0; j < kCached; ++j) asm volatile("" : "+v"(keys[j]));
-  }
-  // ---- ordered write-out
-  int32_t* __restrict__ out = a.idx + (size_t)lh * a.ntot + seq0;
-  const int32_t* __restrict__ sid = a.step_ids + seq0;
-  if (CACHED) {
-    // Flags (1 keep for sure, 2 tie with tau, 4 protected) go through LDS
-    // in batches of 8192 positions so that each thread then holds a run of
-    // 8 consecutive positions per batch; ordered ranks come from two
-    // four-way block scans (one lane of the scan per batch).
-    constexpr int kBatch = 8192, kRun = kBatch / kThreads;  // 8
-    uint8_t* fstage = reinterpret_cast<uint8_t*>(hist);      // 8 KiB of the 12 KiB
-    uint64_t fl[4] = {0ull, 0ull, 0ull, 0ull};
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      if (b * kBatch < ns) {
-#pragma unroll
-        for (int jj = 0; jj < kRun; ++jj) {
-          const int j = kRun * b + jj;
-          const uint32_t key = keys[j];
-          const bool pr = (prot_bits >> j) & 1u;
-          const bool cand = key != 0u;
-          const uint32_t f = (pr || (cand && (take_all || key > tau)) ? 1u : 0u) |
-                             (cand && !take_all && key == tau ? 2u : 0u) | (pr ? 4u : 0u);
-          fstage[tid + kThreads * jj] = (uint8_t)f;
-        }
-        __syncthreads();
-        fl[b] = reinterpret_cast<const uint64_t*>(fstage)[tid];  // positions b*8192 + 8 tid + r
-        __syncthreads();
-      }
-    }
-    auto count_bits = [](uint64_t f, uint64_t m) {
-      return __popcll(f & m);  // one bit per byte selected by m
-    };
-    const uint64_t kOne = 0x0101010101010101ull;
-    int4 nt = make_int4(count_bits(fl[0], 2 * kOne), count_bits(fl[1], 2 * kOne),
-                        count_bits(fl[2], 2 * kOne), count_bits(fl[3], 2 * kOne));
-    int4 tt;
-    const int4 tb = block_exclusive_scan4(nt, scratch, tt);
-    const int tie_off[4] = {tb.x, tt.x + tb.y, tt.x + tt.y + tb.z, tt.x + tt.y + tt.z + tb.w};
-    // keep mask per batch run: byte r set when position 8 tid + r is kept
-    uint32_t keepm[4];
-    int kc[4];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      uint32_t m = 0u;
-      int rank = tie_off[b];
-#pragma unroll
-      for (int r = 0; r < kRun; ++r) {
-        const uint32_t f = (uint32_t)(fl[b] >> (8 * r)) & 0xFFu;
-        bool keep = (f & 1u) != 0u;
-        if (f & 2u) {
-          keep = rank < need;  // ties: lowest positions first
-          ++rank;
-        }
-        m |= (keep ? 1u : 0u) << r;
-      }
-      keepm[b] = m;
-      kc[b] = __popc(m);
-    }
-    int4 kt;
-    const int4 kb = block_exclusive_scan4(make_int4(kc[0], kc[1], kc[2], kc[3]), scratch, kt);
-    const int out_off[4] = {kb.x, kt.x + kb.y, kt.x + kt.y + kb.z, kt.x + kt.y + kt.z + kb.w};
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      int off = out_off[b];
-      uint32_t m = keepm[b];
-      while (m) {
-        const int r = __builtin_ctz(m);
-        m &= m - 1u;
-        out[off++] = kBatch * b + kRun * tid + r;
-      }
-    }
-    if (kept) {
-      // run-length aggregated per thread: consecutive positions share a step
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        uint32_t m = keepm[b];
-        int cur = -1, cnt = 0;
-        while (m) {
-          const int r = __builtin_ctz(m);
-          m &= m - 1u;
-          if ((fl[b] >> (8 * r)) & 4ull) continue;  // protected: no step
-          const int k = sid[kBatch * b + kRun * tid + r];
-          if (k != cur) {
-            if (cur >= 0 && cur < nsteps && cnt) atomicAdd(&kept[cur], cnt);
-            cur = k;
-            cnt = 0;
-          }
-          ++cnt;
-        }
-        if (cur >= 0 && cur < nsteps && cnt) atomicAdd(&kept[cur], cnt);
-      }
-    }
-    return;
-  }
-
+  int32_t* __restrict__ out = a.idx + (size_t)r.lh * a.ntot + r.seq0;
+  const int32_t* __restrict__ sid = a.step_ids + r.seq0;
   int tie_base = 0, out_base = 0;
-  auto emit = [&](int j, uint32_t key) {
+  for (int j = 0; j < nslots; ++j) {
+    const uint32_t key = key_at(j);
     const int par = j & 1;
     const int i = tid + kThreads * j;
     const bool valid = i < ns;
@@ -459,20 +463,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
     }
     if (keep) out[out_base + kb + lanes_below(bk)] = i;
     out_base += kt;
-    if (kept) {
-      const int k = (keep && cand) ? sid[i] : -1;
-      const bool ok = k >= 0 && k < nsteps;
-      uint64_t pend = ballot(ok);
-      while (pend) {
-        const int leader = __builtin_ctzll(pend);
-        const int kk = __shfl(k, leader, kWave);
-        const uint64_t grp = ballot(ok && k == kk);
-        if (lane == leader) atomicAdd(&kept[kk], (int)__popcll(grp));
-        pend &= ~grp;
-      }
-    }
-  };
-  for (int j = 0; j < nslots; ++j) emit(j, key_at(j));
+    if (r.kept) count_kept_steps(r.kept, r.nsteps, (keep && cand) ? sid[i] : -1, lane);
+  }
 }
 
 }  // namespace
@@ -481,9 +473,9 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(retained_plan_kernel, dim3(1), dim3(kThreads), 0, st, a);
   if (a.S * a.LH > 0) {
     if (a.max_len <= kThreads * kCached)
-      hipLaunchKernelGGL(select_kernel<true>, dim3(a.S * a.LH), dim3(kThreads), 0, st, a);
+      hipLaunchKernelGGL(select_cached_kernel, dim3(a.S * a.LH), dim3(kThreads), 0, st, a);
     else
-      hipLaunchKernelGGL(select_kernel<false>, dim3(a.S * a.LH), dim3(kThreads), 0, st, a);
+      hipLaunchKernelGGL(select_stream_kernel, dim3(a.S * a.LH), dim3(kThreads), 0, st, a);
   }
   return hipGetLastError();
 }

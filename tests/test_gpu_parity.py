@@ -247,6 +247,54 @@ def test_token_only_selectors(selector):
     _check_selection(w, g, P32, idx.cpu().numpy(), cu.cpu().numpy(), None)
 
 
+def _special_scores(w, seed):
+    """Priorities that stress the key mapping and the radix search, one pattern per
+    (layer, KV head): NaNs of both signs (quiet and signalling), signed zeros,
+    infinities, subnormals, huge and negative values, all-equal rows, and
+    quantised values with many exact ties."""
+    rng = np.random.default_rng(seed)
+    bits = lambda *u: np.array(u, np.uint32).view(np.float32)
+    nans = bits(0x7FC00000, 0xFFC00000, 0x7F800001, 0xFFBFFFFF)
+    specials = np.concatenate([nans, np.array(
+        [0.0, -0.0, np.inf, -np.inf, 1e-40, -1e-40, 1.4e-45, -1.4e-45, 3e38, -3e38, 0.5, -2.0],
+        np.float32)])
+    n = w.total_tokens
+    pats = [
+        lambda: np.where(rng.random(n) < 0.3, rng.choice(specials, n),
+                         np.round(rng.random(n) * 16) / 8).astype(np.float32),
+        lambda: np.full(n, 0.25, np.float32),                        # every candidate ties
+        lambda: (-np.round(rng.random(n) * 64) / 16 - 1).astype(np.float32),  # negative only
+        lambda: rng.choice(np.array([np.inf, 3e38, 2e38, 1.7014118e38], np.float32), n),
+        lambda: rng.choice(nans, n),                                  # all rank as -inf
+        lambda: rng.random(n).astype(np.float32),
+        lambda: (rng.integers(-5, 6, n) * np.float32(1.4e-45)).astype(np.float32),  # subnormal
+        lambda: rng.choice(specials, n),
+    ]
+    P = np.empty((w.num_layers, w.num_kv_heads, n), np.float32)
+    for lh in range(w.num_layers * w.num_kv_heads):
+        P[lh // w.num_kv_heads, lh % w.num_kv_heads] = pats[lh % len(pats)]()
+    return P
+
+
+@pytest.mark.parametrize("seqlens", [[2500, 700, 130, 1, 0, 4097, 32768], [40000, 3001]],
+                         ids=["registers", "streamed"])
+@pytest.mark.parametrize("budget", [1, 37, 1000])
+def test_select_special_values_bitexact(seqlens, budget):
+    """Selection on crafted fp32 priorities == the oracle's stable ranking of the same numbers
+    (NaN as -inf, -0 as +0), including the kept-per-step counts; sequences up to 32768 tokens
+    take the register path, longer ones the streamed path."""
+    import torch
+
+    w = reduced("ragged16", num_layers=2, seqlens=seqlens, protected_len=64, with_v=False)
+    g = HipRun(w, budget=budget, want_v=False)
+    P = _special_scores(w, 7 + budget)
+    log(f"[special values {seqlens} B={budget}] gpu select")
+    idx, cu_ret, kept = g.select(torch.from_numpy(P).cuda(), want_kept=True)
+    torch.cuda.synchronize()
+    with np.errstate(invalid="ignore"):  # signalling NaNs quieted by the fp64 cast
+        _check_selection(w, g, P, idx.cpu().numpy(), cu_ret.cpu().numpy(), kept.cpu().numpy())
+
+
 def test_repeat_runs_are_bitwise_identical():
     """Fixed reduction orders: repeated runs give identical bits (idx only where defined)."""
     import torch
