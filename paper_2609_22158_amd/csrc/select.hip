@@ -4,8 +4,9 @@
 // Scores map to order-preserving uint32 keys (NaN -> -inf, -0 -> +0). An
 // MSB-first radix select finds the key tau of the B-th largest prunable
 // score and how many tokens equal to tau must be kept; it starts below the
-// bits that every candidate shares (from the block's key min and max) and
-// takes 11-bit digits, so scores spanning a few binades need three passes. The
+// bits that every candidate shares (from the block's key min and max, or from
+// a lower bound for tau and the max) and takes 11-bit digits, so scores
+// spanning a few binades need up to three passes. The
 // write-out walks positions in order: tokens above tau are kept, tokens equal
 // to tau are kept while their rank among equals is below that count (lower
 // positions first), protected tokens are always kept. Histogram increments are
@@ -258,7 +259,7 @@ __global__ __launch_bounds__(kThreads) void retained_plan_kernel(SelectArgs a) {
 // ---------------------------------------------------------------- N_s <= 32768
 __global__ __launch_bounds__(kThreads) void select_cached_kernel(SelectArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t hist[2 * kBins];
-  __shared__ uint32_t red[3][kWaves];
+  __shared__ uint32_t red[5][kWaves];
   __shared__ int sh[2];
 
   const int tid = threadIdx.x;
@@ -296,8 +297,39 @@ __global__ __launch_bounds__(kThreads) void select_cached_kernel(SelectArgs a) {
     kmin1 = min(kmin1, km);
     kmax1 = max(kmax1, keys[j] + 1u);  // kProtKey + 1 wraps to 0
   }
-  // reduced in the shifted domains, where non-candidates lose every min and max
-  reduce_count_range(npr, kmin1, kmax1, red, hist);
+  // A lower bound for tau: each thread holding a candidate has its largest
+  // candidate key (kmax1 - 1), so at least as many candidates as there are such
+  // threads lie at or above the smallest of those maxima; when ktake is within
+  // that number, tau lies there too and the search skips every key below it.
+  const bool has = kmax1 >= 2u;
+  uint32_t tmax = has ? kmax1 - 1u : 0xFFFFFFFFu;
+  const int nthr = __popcll(ballot(has));  // wave total
+  // count, key range and the bound, reduced in one barrier round; kmin1 and
+  // kmax1 in the shifted domains, where non-candidates lose every min and max
+  for (int e = tid; e < kBins; e += kThreads) hist[e] = 0u;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    kmin1 = min(kmin1, (uint32_t)__shfl_xor((int)kmin1, o, kWave));
+    kmax1 = max(kmax1, (uint32_t)__shfl_xor((int)kmax1, o, kWave));
+    tmax = min(tmax, (uint32_t)__shfl_xor((int)tmax, o, kWave));
+  }
+  if (lane == 0) {
+    red[0][wave] = (uint32_t)npr;
+    red[1][wave] = kmin1;
+    red[2][wave] = kmax1;
+    red[3][wave] = tmax;
+    red[4][wave] = (uint32_t)nthr;
+  }
+  __syncthreads();
+  npr = 0;
+  int nthr_all = 0;
+  for (int w = 0; w < kWaves; ++w) {
+    npr += (int)red[0][w];
+    kmin1 = min(kmin1, red[1][w]);
+    kmax1 = max(kmax1, red[2][w]);
+    tmax = min(tmax, red[3][w]);
+    nthr_all += (int)red[4][w];
+  }
   const uint32_t kmin = kmin1 + 1u, kmax = kmax1 - 1u;  // used only when there are candidates
   const int ktake = min(r.B, npr);
   const bool take_all = ktake == npr;
@@ -305,28 +337,24 @@ __global__ __launch_bounds__(kThreads) void select_cached_kernel(SelectArgs a) {
   uint32_t tau = 0u;
   int need = 0;
   if (!take_all) {
-    if (kmin == kmax) {
-      tau = kmin;  // every candidate ties
+    const uint32_t lbound = ktake <= nthr_all ? tmax : kmin;  // tau >= lbound
+    if (lbound == kmax) {
+      tau = kmax;  // every candidate from the bound up ties
       need = ktake;
     } else {
+      const uint32_t span = kmax - lbound;
       auto count = [&](uint32_t* h, uint32_t pmask, uint32_t prefix, int shift, int nbins) {
         // fresh compares in every pass rather than lane masks held across passes
 #pragma unroll
         for (int j = 0; j < kCached; ++j) asm volatile("" : "+v"(keys[j]));
         const uint32_t dm = (uint32_t)(nbins - 1);
-        if (prefix != 0u && prefix != pmask) {
-          // neither 0 nor kProtKey can match the prefix
+        // keys in [lbound, kmax] only: 0 and kProtKey fall outside
 #pragma unroll
-          for (int j = 0; j < kCached; ++j)
-            wave_hist_add(h, (keys[j] & pmask) == prefix, (keys[j] >> shift) & dm, lane);
-        } else {
-#pragma unroll
-          for (int j = 0; j < kCached; ++j)
-            wave_hist_add(h, (keys[j] & pmask) == prefix && keys[j] - 1u < kProtKey - 1u,
-                          (keys[j] >> shift) & dm, lane);
-        }
+        for (int j = 0; j < kCached; ++j)
+          wave_hist_add(h, keys[j] - lbound <= span && (keys[j] & pmask) == prefix,
+                        (keys[j] >> shift) & dm, lane);
       };
-      radix_search(kmin, kmax, ktake, hist, sh, count, tau, need);
+      radix_search(lbound, kmax, ktake, hist, sh, count, tau, need);
     }
   }
 
