@@ -307,7 +307,8 @@ stepkv_problem one_head_view(const stepkv_problem* pb) {
 }
 
 struct SharedLayout {
-  size_t heads, shared, total;  // per-head saliency [n*Hkv][Ntot], summed A [Ntot]
+  size_t heads, shared, cmax, total;  // per-head saliency [n*Hkv][Ntot], summed A [Ntot],
+                                      // chunk maxima of the multi-workgroup priority
 };
 
 SharedLayout shared_layout(const stepkv_problem* pb, int n) {
@@ -316,7 +317,8 @@ SharedLayout shared_layout(const stepkv_problem* pb, int n) {
   SharedLayout w;
   w.heads = layout(&sub, plan_saliency(&sub)).sal;  // after the sweep workspace
   w.shared = align_up(w.heads + sizeof(float) * n * pb->num_kv_heads * ntot);
-  w.total = align_up(w.shared + sizeof(float) * ntot);
+  w.cmax = align_up(w.shared + sizeof(float) * ntot);
+  w.total = align_up(w.cmax + sizeof(float) * shared_chunks(pb->cu_seqlens_host, pb->num_seqs));
   return w;
 }
 
@@ -463,6 +465,27 @@ int stepkv_score_shared(const stepkv_problem* pb, const stepkv_params* prm, cons
                     lse ? SaliencyMode::kFromLse : SaliencyMode::kBoth, lse);
   if (rc != STEPKV_OK) return rc;
   float* sal = saliency ? saliency : reinterpret_cast<float*>(ws + w.shared);
+  if (!step_stats) {
+    // one priority row per sequence, spread over chunks of positions
+    SharedPrioArgs sa;
+    sa.heads = heads;
+    sa.sal = sal;
+    sa.cmax = reinterpret_cast<float*>(ws + w.cmax);
+    sa.cu_seqlens = pb->cu_seqlens;
+    sa.cu_steps = pb->cu_steps;
+    sa.step_ids = step_ids;
+    sa.prot = protected_mask;
+    sa.util = step_utility;
+    sa.scores = scores;
+    sa.S = pb->num_seqs;
+    sa.ntot = ntot;
+    sa.nheads = n * pb->num_kv_heads;
+    sa.half = prm->pool_kernel / 2;
+    sa.alpha = prm->alpha;
+    sa.beta = prm->beta;
+    return hip_status(
+        launch_shared_priority(sa, shared_chunks(pb->cu_seqlens_host, pb->num_seqs), st));
+  }
   rc = hip_status(launch_sum_heads(heads, n * pb->num_kv_heads, ntot, sal, st));
   if (rc != STEPKV_OK) return rc;
   const stepkv_problem one = one_head_view(pb);

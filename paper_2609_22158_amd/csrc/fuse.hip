@@ -351,7 +351,139 @@ __global__ __launch_bounds__(256) void sum_heads_kernel(const float* __restrict_
   out[i] = acc;
 }
 
+// Shared-index mode without step statistics: the single priority row of each
+// sequence is spread over workgroups of kShChunk positions instead of one
+// workgroup per sequence. shared_sum_pool_kernel sums the heads (as
+// sum_heads_kernel does), pools its chunk and writes the chunk's maximum of
+// the pooled prunable values; shared_fuse_kernel takes each sequence's
+// maximum from its chunks' maxima, pools again from the summed saliency and
+// writes P. Both pool in the same order as fuse_batched_kernel (left to
+// right from 0), so the maximum and the values agree bit for bit with it.
+constexpr int kShChunk = 256;
+
+// Chunk g of the concatenated per-sequence chunk lists: sequence s, chunk c.
+__device__ __forceinline__ void shared_chunk(const int32_t* __restrict__ cu_seqlens, int S, int g,
+                                             int& s, int& c, int& cfirst) {
+  int acc = 0;
+  s = S;
+  c = 0;
+  cfirst = 0;
+  for (int t = 0; t < S; ++t) {
+    const int n = cu_seqlens[t + 1] - cu_seqlens[t];
+    const int k = (n + kShChunk - 1) / kShChunk;
+    if (g < acc + k) {
+      s = t;
+      c = g - acc;
+      cfirst = acc;
+      return;
+    }
+    acc += k;
+  }
+}
+
+// Masked (prunable) summed saliency of the chunk and its halos into am[0 ..
+// kShChunk + 2 half): am[e] is position p0 - half + e of the sequence.
+template <bool FROM_HEADS>
+__device__ __forceinline__ void shared_stage(const SharedPrioArgs& a, int seq0, int ns, int p0,
+                                             float* am, float* sum_out) {
+  const int half = a.half;
+  for (int e = threadIdx.x; e < kShChunk + 2 * half; e += kShChunk) {
+    const int p = p0 - half + e;
+    float v = 0.f;
+    if (p >= 0 && p < ns) {
+      const int i = seq0 + p;
+      float acc;
+      if (FROM_HEADS) {  // rows added in row order, eight loads in flight
+        acc = a.heads[i];
+        int h = 1;
+        for (; h + 8 <= a.nheads; h += 8) {
+          float w[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) w[u] = a.heads[(size_t)(h + u) * a.ntot + i];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) acc += w[u];
+        }
+        for (; h < a.nheads; ++h) acc += a.heads[(size_t)h * a.ntot + i];
+        if (e >= half && e < half + kShChunk) sum_out[i] = acc;
+      } else {
+        acc = a.sal[i];
+      }
+      v = a.prot[i] == 0 ? acc : 0.f;
+    }
+    am[e] = v;
+  }
+}
+
+__global__ __launch_bounds__(kShChunk) void shared_sum_pool_kernel(SharedPrioArgs a) {
+  __shared__ float am[kShChunk + 2 * kMaxHalf];
+  __shared__ float wred[kShChunk / kWave];
+  int s, c, cfirst;
+  shared_chunk(a.cu_seqlens, a.S, blockIdx.x, s, c, cfirst);
+  if (s >= a.S) return;  // uniform: the grid holds exactly the chunks
+  const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
+  const int p0 = c * kShChunk;
+  shared_stage<true>(a, seq0, ns, p0, am, a.sal);
+  __syncthreads();
+  const int p = p0 + (int)threadIdx.x;
+  float u = 0.f;
+  for (int o = 0; o <= 2 * a.half; ++o) u += am[threadIdx.x + o];
+  const bool pr = p < ns && a.prot[seq0 + p] == 0;
+  const float m = wave_max(pr ? u : 0.f);  // U >= 0
+  if ((threadIdx.x & 63) == 0) wred[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float mm = 0.f;
+    for (int w = 0; w < kShChunk / kWave; ++w) mm = fmaxf(mm, wred[w]);
+    a.cmax[blockIdx.x] = mm;
+  }
+}
+
+__global__ __launch_bounds__(kShChunk) void shared_fuse_kernel(SharedPrioArgs a) {
+  __shared__ float am[kShChunk + 2 * kMaxHalf];
+  __shared__ float wred[kShChunk / kWave];
+  int s, c, cfirst;
+  shared_chunk(a.cu_seqlens, a.S, blockIdx.x, s, c, cfirst);
+  if (s >= a.S) return;
+  const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
+  const int nch = (ns + kShChunk - 1) / kShChunk;
+  const int p0 = c * kShChunk;
+  // the sequence's maximum over its chunks' maxima
+  float m = 0.f;
+  for (int k = threadIdx.x; k < nch; k += kShChunk) m = fmaxf(m, a.cmax[cfirst + k]);
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) wred[threadIdx.x >> 6] = m;
+  shared_stage<false>(a, seq0, ns, p0, am, nullptr);
+  __syncthreads();
+  float M = 0.f;
+  for (int w = 0; w < kShChunk / kWave; ++w) M = fmaxf(M, wred[w]);
+  const float inv = M > 0.f ? 1.0f / M : 0.f;
+  const int p = p0 + (int)threadIdx.x;
+  if (p >= ns) return;
+  float u = 0.f;
+  for (int o = 0; o <= 2 * a.half; ++o) u += am[threadIdx.x + o];
+  const int i = seq0 + p;
+  const bool pr = a.prot[i] == 0;
+  const int st0 = a.cu_steps[s], nsteps = a.cu_steps[s + 1] - st0;
+  const int kk = a.step_ids[i];
+  const bool ok = pr && kk >= 0 && kk < nsteps;
+  const float util = ok ? a.util[st0 + kk] : 0.f;
+  a.scores[i] = pr ? fmaf(a.alpha, u * inv, a.beta * util) : -INFINITY;
+}
+
 }  // namespace
+
+int shared_chunks(const int32_t* cu_seqlens_host, int S) {
+  int n = 0;
+  for (int t = 0; t < S; ++t) n += (cu_seqlens_host[t + 1] - cu_seqlens_host[t] + kShChunk - 1) / kShChunk;
+  return n;
+}
+
+hipError_t launch_shared_priority(const SharedPrioArgs& a, int chunks, hipStream_t st) {
+  if (chunks == 0) return hipSuccess;
+  hipLaunchKernelGGL(shared_sum_pool_kernel, dim3(chunks), dim3(kShChunk), 0, st, a);
+  hipLaunchKernelGGL(shared_fuse_kernel, dim3(chunks), dim3(kShChunk), 0, st, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_sum_heads(const float* sal, int heads, int ntot, float* out, hipStream_t st) {
   if (ntot == 0 || heads == 0) return hipSuccess;

@@ -49,6 +49,23 @@ struct FuseArgs {
   float alpha, beta;
 };
 hipError_t launch_fuse(const FuseArgs& a, hipStream_t st);
+
+// Shared-index priority without step statistics, over chunks of 256 positions.
+struct SharedPrioArgs {
+  const float* heads;        // [nheads][Ntot] per-head saliency of the last layers
+  float* sal;                // [Ntot] summed saliency (written by the first kernel)
+  float* cmax;               // [chunks] maximum pooled prunable value per chunk
+  const int32_t* cu_seqlens; // [S+1]
+  const int32_t* cu_steps;   // [S+1]
+  const int32_t* step_ids;   // [Ntot]
+  const uint8_t* prot;       // [Ntot]
+  const float* util;         // [cu_steps[S]]
+  float* scores;             // [Ntot]
+  int S, ntot, nheads, half;
+  float alpha, beta;
+};
+int shared_chunks(const int32_t* cu_seqlens_host, int S);
+hipError_t launch_shared_priority(const SharedPrioArgs& a, int chunks, hipStream_t st);
 // out[i] = sum over h < heads of sal[h][i] (fp32, [heads][ntot] -> [ntot]).
 hipError_t launch_sum_heads(const float* sal, int heads, int ntot, float* out, hipStream_t st);
 

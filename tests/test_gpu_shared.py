@@ -51,6 +51,26 @@ def _seqs(w):
 
 
 @pytest.mark.parametrize("cid", list(CASES))
+def test_shared_priority_paths_agree(cid):
+    """Without step statistics the priority row of a sequence is spread over many workgroups;
+    with them one workgroup per sequence also forms the statistics. Both give the same summed
+    saliency and priorities bit for bit, and the statistics count every prunable token once."""
+    w, g, sc, o = _case(cid)
+    log(f"[shared {cid}] with step statistics")
+    sc2 = B.score_shared(g.pb, g.q, g.k, g.sid, g.prot, g.util, g.params, last_layers=LAST,
+                         want_saliency=True, want_stats=True)
+    assert np.array_equal(sc2["saliency"].cpu().numpy(), sc["saliency"].cpu().numpy())
+    assert np.array_equal(sc2["scores"].cpu().numpy(), sc["scores"].cpu().numpy())
+    cnt = B.decode_stats(sc2["stats_raw"])["count"].reshape(-1)
+    for s, a, b in _seqs(w):
+        k0, k1 = int(w.cu_steps[s]), int(w.cu_steps[s + 1])
+        prun = w.protected[a:b] == 0
+        sid = w.step_ids[a:b]
+        want = np.bincount(sid[prun & (sid >= 0) & (sid < k1 - k0)], minlength=k1 - k0)
+        assert np.array_equal(cnt[k0:k1], want), f"counts seq {s}"
+
+
+@pytest.mark.parametrize("cid", list(CASES))
 def test_shared_scores_match_oracle(cid):
     w, g, sc, o = _case(cid)
     P = sc["scores"].cpu().numpy()
