@@ -70,6 +70,20 @@ def test_shared_priority_paths_agree(cid):
         assert np.array_equal(cnt[k0:k1], want), f"counts seq {s}"
 
 
+@pytest.mark.parametrize("pool", [1, 63])
+def test_shared_priority_paths_agree_any_pool(pool):
+    """The two shared-index priority paths at the smallest and largest pooling windows (a
+    halo of 31 positions on each side of a 256-position chunk)."""
+    cid = list(CASES)[-1]
+    w, g, _, _ = _case(cid)
+    p = B.Params(pool_kernel=pool)
+    log(f"[shared {cid}] pool {pool}, both priority paths")
+    a = B.score_shared(g.pb, g.q, g.k, g.sid, g.prot, g.util, p, last_layers=LAST)
+    b = B.score_shared(g.pb, g.q, g.k, g.sid, g.prot, g.util, p, last_layers=LAST,
+                       want_stats=True)
+    assert np.array_equal(a["scores"].cpu().numpy(), b["scores"].cpu().numpy())
+
+
 @pytest.mark.parametrize("cid", list(CASES))
 def test_shared_scores_match_oracle(cid):
     w, g, sc, o = _case(cid)
