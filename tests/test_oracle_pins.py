@@ -377,6 +377,19 @@ def test_kept_per_step_sums_to_kept():
     assert (st["count"] == 9).all()
 
 
+def test_step_statistics_hand_values():
+    """Per-step diagnostics (the token counts and saliency mass behind Figs. 2 and 8) on a
+    hand-worked example: a protected token, an id of -1 and an id past the step count are
+    left out; values worked out by hand."""
+    T_hat = np.array([0.5, 0.2, 0.9, 0.1, 0.4, 0.7, 0.3])
+    sid = np.array([0, 0, 1, 1, -1, 5, 1])
+    prun = np.array([True, False, True, True, True, True, True])
+    st = O.step_statistics(T_hat, sid, prun, 2)
+    assert list(st["count"]) == [1, 3]
+    assert np.allclose(st["max"], [0.5, 0.9], rtol=0, atol=1e-15)
+    assert np.allclose(st["sum"], [0.5, 1.3], rtol=0, atol=1e-15)
+
+
 # ------------------------------------------------------------- compaction, decode
 def test_compact_is_row_gather():
     rng = np.random.default_rng(4)
