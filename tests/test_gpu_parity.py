@@ -247,6 +247,33 @@ def test_token_only_selectors(selector):
     _check_selection(w, g, P32, idx.cpu().numpy(), cu.cpu().numpy(), None)
 
 
+@pytest.mark.parametrize("pool", [7, 15])
+def test_long_sequence_and_wide_pool_match_oracle(pool):
+    """A 40000-token sequence (past the 32768 the register paths hold) and a pooling window of
+    15 (past the 9 of the batched priority kernel) take the streamed priority kernel; scores,
+    saliency and step statistics against the oracle."""
+    from paper_2609_22158_amd import binding as B
+
+    w = reduced("ragged16", num_layers=1, seqlens=[40000, 333], protected_len=64, num_steps=30)
+    p = B.Params(pool_kernel=pool)
+    g = HipRun(w, params=p, want_v=False)
+    log(f"[long sequence pool {pool}] gpu score")
+    sc = g.score(want_saliency=True, want_stats=True)
+    o = run_oracle(w, g.budget, p)
+    P = sc["scores"].cpu().numpy()
+    A = sc["saliency"].cpu().numpy()
+    st = B.decode_stats(sc["stats_raw"])
+    for s, l, h, a, b in _heads(w):
+        close(A[l, h, a:b], o["A"][(s, l, h)], f"A{(s, l, h)}")
+        close(P[l, h, a:b], o["P"][(s, l, h)], f"P{(s, l, h)}")
+        k0, k1 = int(w.cu_steps[s]), int(w.cu_steps[s + 1])
+        prun = w.protected[a:b] == 0
+        ref = O.step_statistics(o["T_hat"][(s, l, h)], w.step_ids[a:b], prun, k1 - k0)
+        assert np.array_equal(st["count"][l, h, k0:k1], ref["count"])
+        np.testing.assert_allclose(st["max"][l, h, k0:k1], ref["max"], rtol=2e-3, atol=1e-6)
+        np.testing.assert_allclose(st["sum"][l, h, k0:k1], ref["sum"], rtol=2e-3, atol=1e-4)
+
+
 def _special_scores(w, seed):
     """Priorities that stress the key mapping and the radix search, one pattern per
     (layer, KV head): NaNs of both signs (quiet and signalling), signed zeros,
