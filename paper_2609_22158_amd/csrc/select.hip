@@ -222,37 +222,70 @@ __device__ __forceinline__ RowSetup row_setup(const SelectArgs& a) {
   return r;
 }
 
+// Protected tokens of sequence s, counted by the whole workgroup: 16 at a
+// time from aligned 16-byte words, the unaligned head and tail one byte at a
+// time.
+__device__ int count_protected(const SelectArgs& a, int s, int* scratch) {
+  const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
+  const int misal = (int)(reinterpret_cast<uintptr_t>(a.prot + seq0) & 15);
+  const int head = min(ns, (16 - misal) & 15);
+  const int nvec = (ns - head) / 16;
+  int np = 0;
+  if ((int)threadIdx.x < head) np += a.prot[seq0 + threadIdx.x] != 0;
+  const uint4* vp = reinterpret_cast<const uint4*>(a.prot + seq0 + head);
+  for (int i = threadIdx.x; i < nvec; i += kThreads) {
+    const uint4 w = vp[i];
+    const uint32_t x[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {  // one bit per nonzero byte
+      uint32_t b = x[c] | (x[c] >> 4);
+      b |= b >> 2;
+      b |= b >> 1;
+      np += __builtin_popcount(b & 0x01010101u);
+    }
+  }
+  for (int i = head + 16 * nvec + threadIdx.x; i < ns; i += kThreads) np += a.prot[seq0 + i] != 0;
+  return block_sum_int(np, scratch);
+}
+
+__device__ __forceinline__ int budget_of(const SelectArgs& a, int s) {
+  return a.budgets ? max(1, a.budgets[s]) : a.budget;
+}
+
 // cu_retained[s+1] - cu_retained[s] = n_protected_s + min(B_s, N_s - n_protected_s)
+// Without heads there are no selection workgroups; one workgroup writes the plan.
 __global__ __launch_bounds__(kThreads) void retained_plan_kernel(SelectArgs a) {
   __shared__ int scratch[kWaves];
   int acc = 0;
   if (threadIdx.x == 0) a.cu_retained[0] = 0;
   for (int s = 0; s < a.S; ++s) {
-    const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
-    // protected flags counted 16 at a time from aligned 16-byte words; the
-    // unaligned head and tail one byte at a time
-    const int misal = (int)(reinterpret_cast<uintptr_t>(a.prot + seq0) & 15);
-    const int head = min(ns, (16 - misal) & 15);
-    const int nvec = (ns - head) / 16;
-    int np = 0;
-    if ((int)threadIdx.x < head) np += a.prot[seq0 + threadIdx.x] != 0;
-    const uint4* vp = reinterpret_cast<const uint4*>(a.prot + seq0 + head);
-    for (int i = threadIdx.x; i < nvec; i += kThreads) {
-      const uint4 w = vp[i];
-      const uint32_t x[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {  // one bit per nonzero byte
-        uint32_t b = x[c] | (x[c] >> 4);
-        b |= b >> 2;
-        b |= b >> 1;
-        np += __builtin_popcount(b & 0x01010101u);
-      }
-    }
-    for (int i = head + 16 * nvec + threadIdx.x; i < ns; i += kThreads) np += a.prot[seq0 + i] != 0;
-    np = block_sum_int(np, scratch);
-    const int B = a.budgets ? max(1, a.budgets[s]) : a.budget;
-    acc += np + min(B, ns - np);
+    const int ns = a.cu_seqlens[s + 1] - a.cu_seqlens[s];
+    const int np = count_protected(a, s, scratch);
+    acc += np + min(budget_of(a, s), ns - np);
     if (threadIdx.x == 0) a.cu_retained[s + 1] = acc;
+  }
+}
+
+// The same plan from the selection workgroups of head 0: the workgroup of
+// sequence s counts the protected tokens of the sequences before it (none
+// with a single sequence) before it loads its keys, and adds its own
+// sequence once its candidate count npr = N_s - n_protected_s is known.
+// Block-uniform: only the head-0 workgroups call these.
+__device__ int retained_before(const SelectArgs& a, int s, int* scratch) {
+  int acc = 0;
+  for (int t = 0; t < s; ++t) {
+    const int nt = a.cu_seqlens[t + 1] - a.cu_seqlens[t];
+    const int np = count_protected(a, t, scratch);
+    acc += np + min(budget_of(a, t), nt - np);
+  }
+  return acc;
+}
+
+__device__ __forceinline__ void write_retained(const SelectArgs& a, int s, int before, int ns,
+                                               int npr, int B) {
+  if (threadIdx.x == 0) {
+    if (s == 0) a.cu_retained[0] = 0;
+    a.cu_retained[s + 1] = before + (ns - npr) + min(B, npr);
   }
 }
 
@@ -261,6 +294,7 @@ __global__ __launch_bounds__(kThreads) void select_cached_kernel(SelectArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t hist[2 * kBins];
   __shared__ uint32_t red[5][kWaves];
   __shared__ int sh[2];
+  __shared__ int plan_scratch[kWaves];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -268,6 +302,7 @@ __global__ __launch_bounds__(kThreads) void select_cached_kernel(SelectArgs a) {
   const int ns = r.ns;
   const float* __restrict__ P = a.scores + (size_t)r.lh * a.ntot + r.seq0;
   const uint8_t* __restrict__ prot = a.prot + r.seq0;
+  const int plan_before = r.lh == 0 ? retained_before(a, r.s, plan_scratch) : 0;
 
   // every load issued before any is used: indices clamped into the sequence
   float pv[kCached];
@@ -333,6 +368,7 @@ __global__ __launch_bounds__(kThreads) void select_cached_kernel(SelectArgs a) {
   const uint32_t kmin = kmin1 + 1u, kmax = kmax1 - 1u;  // used only when there are candidates
   const int ktake = min(r.B, npr);
   const bool take_all = ktake == npr;
+  if (r.lh == 0) write_retained(a, r.s, plan_before, ns, npr, r.B);
 
   uint32_t tau = 0u;
   int need = 0;
@@ -413,6 +449,7 @@ __global__ __launch_bounds__(kThreads) void select_stream_kernel(SelectArgs a) {
   __shared__ uint32_t red[3][kWaves];
   __shared__ int wcnt[2][2][kWaves];
   __shared__ int sh[2];
+  __shared__ int plan_scratch[kWaves];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -420,6 +457,7 @@ __global__ __launch_bounds__(kThreads) void select_stream_kernel(SelectArgs a) {
   const int ns = r.ns;
   const float* __restrict__ P = a.scores + (size_t)r.lh * a.ntot + r.seq0;
   const uint8_t* __restrict__ prot = a.prot + r.seq0;
+  const int plan_before = r.lh == 0 ? retained_before(a, r.s, plan_scratch) : 0;
   // position of slot j of this thread: tid + kThreads * j (coalesced)
   auto key_at = [&](int j) -> uint32_t {
     const int i = tid + kThreads * j;
@@ -439,6 +477,7 @@ __global__ __launch_bounds__(kThreads) void select_stream_kernel(SelectArgs a) {
   reduce_count_range(npr, kmin, kmax, red, hist);
   const int ktake = min(r.B, npr);
   const bool take_all = ktake == npr;
+  if (r.lh == 0) write_retained(a, r.s, plan_before, ns, npr, r.B);
 
   uint32_t tau = 0u;
   int need = 0;
@@ -498,8 +537,9 @@ __global__ __launch_bounds__(kThreads) void select_stream_kernel(SelectArgs a) {
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(retained_plan_kernel, dim3(1), dim3(kThreads), 0, st, a);
-  if (a.S * a.LH > 0) {
+  if (a.S * a.LH == 0) {
+    hipLaunchKernelGGL(retained_plan_kernel, dim3(1), dim3(kThreads), 0, st, a);
+  } else {
     if (a.max_len <= kThreads * kCached)
       hipLaunchKernelGGL(select_cached_kernel, dim3(a.S * a.LH), dim3(kThreads), 0, st, a);
     else
