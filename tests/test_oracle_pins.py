@@ -24,6 +24,44 @@ def bits(x):
     return f32_to_bf16_bits(np.asarray(x, dtype=np.float32))
 
 
+# ------------------------------------------------------------- bf16 decoding
+# Hand-decoded bf16 bit patterns: sign bit 15, exponent bits 14-7 (bias 127),
+# mantissa bits 6-0; exponent 0 is subnormal (2^-126 * m/128), 255 is inf/NaN.
+BF16_HAND = [
+    (0x3F80, 1.0),
+    (0x3F00, 0.5),
+    (0xC000, -2.0),
+    (0xC020, -2.5),  # exponent 128, mantissa 0x20 -> -(1 + 32/128) * 2
+    (0x4049, 3.140625),  # exponent 128, mantissa 73 -> (1 + 73/128) * 2
+    (0x0080, math.ldexp(1.0, -126)),  # smallest normal
+    (0x0001, math.ldexp(1.0, -133)),  # smallest subnormal: 2^-126 / 128
+    (0x807F, -math.ldexp(127.0, -133)),  # largest negative subnormal
+    (0x7F7F, math.ldexp(255.0, 120)),  # largest finite: (255/128) * 2^127
+    (0x7F80, math.inf),
+    (0xFF80, -math.inf),
+    (0x0000, 0.0),
+]
+
+
+def test_decode_bf16_hand_bit_patterns():
+    """bf16 is the top half of an IEEE binary32 word; every value is exact in fp64."""
+    raw = np.array([b for b, _ in BF16_HAND], dtype=np.uint16)
+    got = O.decode_bf16(raw)
+    assert got.dtype == np.float64
+    for (b, want), g in zip(BF16_HAND, got):
+        assert g == want, f"0x{b:04X}: {g!r} != {want!r}"
+    neg_zero = O.decode_bf16(np.array([0x8000], dtype=np.uint16))[0]
+    assert neg_zero == 0.0 and math.copysign(1.0, neg_zero) == -1.0
+    for b in (0x7FC0, 0xFFC1, 0x7F81):  # quiet, negative and signalling NaN payloads
+        assert math.isnan(O.decode_bf16(np.array([b], dtype=np.uint16))[0])
+    # the shape is kept and element order follows the array, not the bytes
+    grid = raw[:12].reshape(3, 4)
+    np.testing.assert_array_equal(O.decode_bf16(grid), got[:12].reshape(3, 4))
+    # the round trip through the generators' RNE encoder on values exact in bf16
+    vals = np.array([w for _, w in BF16_HAND if math.isfinite(w)], dtype=np.float32)
+    np.testing.assert_array_equal(O.decode_bf16(bits(vals)), vals.astype(np.float64))
+
+
 # ------------------------------------------------------------- step utility
 def _golden_cases():
     with open(os.path.join(GOLDEN, "step_utility.json")) as f:
@@ -377,6 +415,24 @@ def test_kept_per_step_sums_to_kept():
     assert (st["count"] == 9).all()
 
 
+def test_kept_per_step_hand_values():
+    """Retained prunable tokens per step (the per-step view behind Figs. 2 and 8), worked
+    out by hand: protected tokens, a prunable token with id -1 and one with an id past the
+    step count are retained but counted in no step."""
+    #            pos: 0   1   2  3  4  5  6  7  8  9  10 11
+    sid = np.array([-1, -1, 0, 0, 1, 1, 1, 2, 5, 0, 2, -1])
+    prun = np.array([0, 1, 1, 1, 1, 1, 1, 1, 1, 0, 1, 1], bool)
+    idx = np.array([0, 1, 3, 4, 6, 7, 8, 9, 10])
+    # step 0: pos 3 (pos 9 is protected); step 1: pos 4 and 6; step 2: pos 7 and 10;
+    # pos 0 (protected, -1), 1 (prunable, -1) and 8 (id 5 >= 3) count nowhere
+    np.testing.assert_array_equal(O.kept_per_step(idx, sid, prun, 3), [1, 2, 2])
+    np.testing.assert_array_equal(O.kept_per_step(idx, sid, prun, 6), [1, 2, 2, 0, 0, 1])
+    np.testing.assert_array_equal(O.kept_per_step(idx[:0], sid, prun, 3), [0, 0, 0])
+    # every prunable token of steps 0..2 retained: the counts are the step lengths
+    all_idx = np.arange(12)
+    np.testing.assert_array_equal(O.kept_per_step(all_idx, sid, prun, 3), [2, 3, 2])
+
+
 def test_step_statistics_hand_values():
     """Per-step diagnostics (the token counts and saliency mass behind Figs. 2 and 8) on a
     hand-worked example: a protected token, an id of -1 and an id past the step count are
@@ -412,6 +468,128 @@ def test_decode_attention_matches_torch_sdpa():
     np.testing.assert_allclose(O.decode_attention(q, K, V, 1 / 8), ref, rtol=1e-12)
     # one retained row: the output is that value row
     np.testing.assert_allclose(O.decode_attention(q, K[:1], V[:1], 1 / 8), V[0], rtol=1e-15)
+
+
+# ------------------------------------------------------------- batched sequences
+def _batch_case(lens=(70, 0, 1, 95), steps=(5, 1, 1, 7), prot_len=(6, 0, 1, 9), L=2, Hkv=2,
+                G=3, W=4, d=64, seed=21):
+    """A ragged batch in the library's layout: sequences concatenated along the token axis,
+    step utilities concatenated along cu_steps, one q_win / lse_win slice per sequence."""
+    rng = np.random.default_rng(seed)
+    nseq, ntot = len(lens), sum(lens)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    cs = np.concatenate([[0], np.cumsum(steps)]).astype(np.int64)
+    q = bits(rng.standard_normal((L, nseq, W, Hkv * G, d)))
+    k = bits(rng.standard_normal((L, Hkv, ntot, d)) / math.sqrt(d))
+    v = bits(rng.standard_normal((L, Hkv, ntot, d)))
+    sid = np.full(ntot, -1, np.int32)
+    prot = np.zeros(ntot, np.uint8)
+    for s in range(nseq):
+        a, b = int(cu[s]), int(cu[s + 1])
+        prot[a:a + prot_len[s]] = 1
+        n_pr = b - a - prot_len[s]
+        if n_pr > 0:
+            sid[a + prot_len[s]:b] = np.sort(rng.integers(0, steps[s], n_pr))
+    S = rng.uniform(0.0, 1.7, int(cs[-1]))
+    lse = rng.normal(2.0, 0.5, (L, nseq, W, Hkv * G))  # not the exact LSE: each row's
+    return q, k, v, cu, sid, prot, cs, S, lse          # value changes its contribution
+
+
+def _alone(case, s):
+    """Sequence s of a batch as a one-sequence problem."""
+    q, k, v, cu, sid, prot, cs, S, lse = case
+    a, b = int(cu[s]), int(cu[s + 1])
+    return (q[:, s:s + 1], k[:, :, a:b], v[:, :, a:b], np.array([0, b - a]), sid[a:b],
+            prot[a:b], np.array([0, cs[s + 1] - cs[s]]), S[cs[s]:cs[s + 1]], lse[:, s:s + 1])
+
+
+@pytest.mark.parametrize("mode", ["two-sweep", "lse-fed", "causal"])
+def test_compress_batch_equals_each_sequence_alone(mode):
+    """eq. problem holds per sequence: on a ragged batch, the pass over the concatenated
+    layout (cu_seqlens, cu_steps, the sequence's q_win / lse_win slice) gives for every
+    sequence what the pass over that sequence alone gives: P, A, T_hat, idx, kept, K_hat, V_hat."""
+    case = _batch_case()
+    q, k, v, cu, sid, prot, cs, S, lse = case
+    p = O.Params(causal_tail=(mode == "causal"))
+    use_lse = mode == "lse-fed"
+    batch = O.compress(q, k, v, cu, sid, prot, cs, S, 9, p, want_saliency=True,
+                       lse_win=lse if use_lse else None)
+    seen = 0
+    for s in range(len(cu) - 1):
+        q1, k1, v1, cu1, sid1, prot1, cs1, S1, lse1 = _alone(case, s)
+        one = O.compress(q1, k1, v1, cu1, sid1, prot1, cs1, S1, 9, p, want_saliency=True,
+                         lse_win=lse1 if use_lse else None)
+        for l in range(q.shape[0]):
+            for h in range(k.shape[1]):
+                got, want = (s, l, h), (0, l, h)
+                for f in ("P", "A", "T_hat"):
+                    np.testing.assert_array_equal(batch[f][got], one[f][want], err_msg=f)
+                for f in ("idx", "kept"):
+                    np.testing.assert_array_equal(batch[f][got], one[f][want], err_msg=f)
+                for f, src in (("k_hat", k1), ("v_hat", v1)):  # an empty cache stores none
+                    want_rows = one[f].get(want, src[l, h][one["idx"][want]])
+                    np.testing.assert_array_equal(batch[f][got], want_rows, err_msg=f)
+                seen += 1
+    assert seen == 4 * 2 * 2
+    a3 = int(cu[3])
+    assert len(batch["idx"][(3, 1, 1)]) == 9 + 9 and batch["idx"][(1, 0, 0)].size == 0
+    assert list(batch["idx"][(2, 0, 0)]) == [0]  # one protected token, nothing prunable
+    assert batch["kept"][(3, 0, 0)].sum() == 9 and len(batch["kept"][(3, 0, 0)]) == 7
+    np.testing.assert_array_equal(batch["k_hat"][(3, 1, 0)],
+                                  k[1, 0, a3:][batch["idx"][(3, 1, 0)]])
+
+
+def test_compress_batch_uses_each_sequences_own_slices():
+    """The per-sequence slices are not interchangeable: changing sequence 3's window
+    queries, utilities or row LSEs changes sequence 3's result and no other."""
+    case = _batch_case()
+    q, k, v, cu, sid, prot, cs, S, lse = case
+    base = O.compress(q, k, v, cu, sid, prot, cs, S, 9, want_saliency=True, lse_win=lse)
+    q2 = q.copy()
+    q2[:, 3] = bits(np.random.default_rng(7).standard_normal(q2[:, 3].shape))
+    S2 = S.copy()
+    S2[cs[3]:cs[4]] = S2[cs[3]:cs[4]][::-1] + 0.05
+    lse2 = lse.copy()
+    lse2[:, 3] += np.random.default_rng(8).normal(0, 1, lse2[:, 3].shape)
+    for kw in ({"q_win": q2}, {"S": S2}, {"lse_win": lse2}):
+        args = dict(q_win=q, k=k, v=v, cu_seqlens=cu, step_ids=sid, protected=prot,
+                    cu_steps=cs, S=S, budget=9, want_saliency=True, lse_win=lse)
+        args.update(kw)
+        out = O.compress(**args)
+        for key in base["P"]:
+            same = np.array_equal(out["P"][key], base["P"][key])
+            assert same == (key[0] != 3), (list(kw), key)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_compress_lse_fed_with_library_lse_equals_two_sweeps(causal):
+    """App. C.2: given every window row's exact log-sum-exp in the lse_win layout
+    [L][S][W][Hq] (scipy's logsumexp over the keys the row sees, per sequence), the
+    LSE-fed pass equals the two-sweep pass on every sequence, layer and KV head."""
+    q, k, v, cu, sid, prot, cs, S, _ = _batch_case()
+    L, nseq, W, Hq, d = q.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    qf, kf = O.decode_bf16(q), O.decode_bf16(k)
+    lse = np.full((L, nseq, W, Hq), -np.inf)
+    for l in range(L):
+        for s in range(nseq):
+            a, b = int(cu[s]), int(cu[s + 1])
+            n = b - a
+            for w in range(W):
+                last = n - W + w if causal else n - 1  # the last key slot w sees
+                for hq in range(Hq):
+                    if last < 0 or n == 0:
+                        continue
+                    z = kf[l, hq // G, a:a + last + 1] @ qf[l, s, w, hq] / math.sqrt(d)
+                    lse[l, s, w, hq] = scipy.special.logsumexp(z)
+    p = O.Params(causal_tail=causal)
+    two = O.compress(q, k, v, cu, sid, prot, cs, S, 9, p, want_saliency=True)
+    fed = O.compress(q, k, v, cu, sid, prot, cs, S, 9, p, want_saliency=True, lse_win=lse)
+    for key in two["P"]:
+        np.testing.assert_allclose(fed["A"][key], two["A"][key], rtol=1e-12, atol=1e-300)
+        np.testing.assert_allclose(fed["P"][key], two["P"][key], rtol=1e-12)
+        np.testing.assert_array_equal(fed["idx"][key], two["idx"][key])
 
 
 # ------------------------------------------------------------- shared-index mode
