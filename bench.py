@@ -308,7 +308,7 @@ def main():
     scores = torch.empty_like(sal)
     idx = torch.empty((L, Hkv, ntot), dtype=torch.int32, device=dev)
     cu_ret = torch.empty(w.num_seqs + 1, dtype=torch.int32, device=dev)
-    out_rows = B.retained_rows(w.seqlens, w.protected_len, budget)
+    out_rows = int(pb.retained_rows(w.protected, budget)[-1])
     k_out = torch.empty((L, Hkv, out_rows, d), dtype=torch.bfloat16, device=dev)
     v_out = torch.empty_like(k_out)
     ws = torch.empty(pb.saliency_workspace_bytes(), dtype=torch.uint8, device=dev)

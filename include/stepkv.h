@@ -37,6 +37,10 @@
  *  - Arguments are validated on the host before anything is launched; a
  *    failed validation returns an error code and launches nothing.
  *  - No C++ exception crosses this interface.
+ *  - Conditions only the device can see (a step id out of range, a
+ *    non-finite input, rows past out_rows) are reported through the
+ *    problem's optional status word (stepkv_problem.status,
+ *    stepkv_status_read), not through return codes.
  *
  * Layouts (L layers, S sequences, Hq query heads, Hkv KV heads, G = Hq/Hkv,
  * d head dim, W window length, Ntot = cu_seqlens[S]):
@@ -79,6 +83,16 @@ extern "C" {
 #define STEPKV_MAX_STEPS_STATS 4096  /* steps per sequence when stats are requested */
 #define STEPKV_CUE_CAP 64            /* evidence cues per text field (App. D) */
 
+/* Conditions the kernels detect on the device (stepkv_problem.status). None
+ * stops a call: each result stays defined as the call's text says. */
+#define STEPKV_FLAG_STEP_ID 1u   /* a prunable token's step id lies outside [0, n_steps_s):
+                                    it took utility 0 (priority, score calls) */
+#define STEPKV_FLAG_NONFINITE 2u /* a prunable token's saliency or step utility was NaN or
+                                    infinite (NaN or inf in q_win, k, lse_win or
+                                    step_utility); its priority is not finite */
+#define STEPKV_FLAG_OUT_ROWS 4u  /* cu_retained[S] exceeded out_rows: rows at or past
+                                    out_rows were not written (compact) or read (decode) */
+
 /* ---------------------------------------------------------------- types */
 /* Shape of one compression problem: a batch of S sequences, all layers. */
 typedef struct stepkv_problem {
@@ -92,6 +106,12 @@ typedef struct stepkv_problem {
   const int32_t* cu_seqlens;      /* [S+1] device copy of the same values */
   const int32_t* cu_steps_host;   /* [S+1] host: offsets into step_utility */
   const int32_t* cu_steps;        /* [S+1] device copy of the same values */
+  /* Device status word (uint32 [1], caller-owned) or NULL. When set, the
+   * kernels of every device call on this problem OR the STEPKV_FLAG_* bits of
+   * the conditions they meet into it; nothing else writes it. The caller
+   * zeroes it once (or through stepkv_status_read) and reads it back with
+   * stepkv_status_read. Calls that may run at the same time share it. */
+  uint32_t* status;
 } stepkv_problem;
 
 /* Method parameters; stepkv_params_default() fills the paper's defaults
@@ -145,6 +165,29 @@ const char* stepkv_strerror(int code);
 /* eq. problem: B = max(1, floor(rho * n_prunable)), rho in (0, 1].
  * Returns -1 for rho outside (0, 1] or n_prunable < 0. */
 int64_t stepkv_budget_from_ratio(double rho, int64_t n_prunable);
+
+/* eq. problem, with exactly min(B_s, N_pr,s) prunable tokens kept (Algorithm 1
+ * output): the compacted rows of every sequence,
+ *   R_s = P_s + min(B_s, N_s - P_s),  P_s = protected tokens of sequence s,
+ * prefix-summed into cu_retained_host [S+1] (host); cu_retained_host[S] is
+ * the out_rows that stepkv_compact needs. B_s is `budget`, or
+ * max(1, budgets_host[s]) when budgets_host (host int32 [S]) is non-NULL:
+ * the same rule, clamp included, as stepkv_select, whose cu_retained equals
+ * this result. protected_host is the host copy of the protected mask, uint8
+ * [cu_seqlens_host[S]] (nonzero = protected). Host only.
+ * Errors: EINVAL for a null or bad problem, null protected_host or
+ * cu_retained_host, budget < 1 without budgets_host, or a total beyond
+ * INT32_MAX. */
+int stepkv_retained_rows(const stepkv_problem* pb, const uint8_t* protected_host, int32_t budget,
+                         const int32_t* budgets_host, int32_t* cu_retained_host);
+
+/* Reads the problem's device status word (pb->status) after the work queued
+ * on `stream` so far has finished (the call waits for the stream), into
+ * *flags_host, and sets it to zero when `clear` is nonzero (on the stream,
+ * waited for). The call synchronizes, so it does not belong inside a
+ * captured HIP graph. Errors: EINVAL (null pb, pb->status or flags_host),
+ * EHIP. */
+int stepkv_status_read(const stepkv_problem* pb, uint32_t* flags_host, int32_t clear, void* stream);
 
 /* Algorithm 1 phases 1-2 at the boundary after step t = state->num_steps + 1.
  * Phase 1: r_t = valid + gain - lambda*red (eq. reward; for the first step
@@ -351,12 +394,40 @@ int stepkv_select(const stepkv_problem* pb, const float* scores, const uint8_t* 
 /* eq. problem: C_hat = C_prot || C_traj[K]. For every (l, h) and sequence s,
  * k_out[l][h][cu_retained[s] + j] = k[l][h][cu_seqlens[s] + idx[l][h][cu_seqlens[s] + j]]
  * for j < R_s, and likewise v. Rows at or beyond out_rows are not written
- * (cu_retained[S] gives the rows needed). A bit-exact copy; the outputs must
- * not overlap the inputs. Errors: EINVAL for null pointers, a bad problem or
- * out_rows < 0; EHIP on launch failure. */
+ * (cu_retained[S] gives the rows needed; stepkv_retained_rows computes it on
+ * the host) and STEPKV_FLAG_OUT_ROWS is set in pb->status when rows were
+ * dropped. A bit-exact copy; the outputs must
+ * not overlap the inputs; k_out and v_out may be NULL when out_rows is 0.
+ * Errors: EINVAL for null pointers, a bad problem or out_rows < 0; EHIP on
+ * launch failure. */
 int stepkv_compact(const stepkv_problem* pb, const void* k, const void* v, const int32_t* idx,
                    const int32_t* cu_retained, int32_t out_rows, void* k_out, void* v_out,
                    void* stream);
+
+/* Bytes of device workspace stepkv_compress needs (0 when invalid): the score
+ * workspace plus room for the scores and the retained positions, used when
+ * the caller passes NULL for them. 256-byte alignment is required. */
+size_t stepkv_compress_workspace_bytes(const stepkv_problem* pb);
+
+/* The whole pass at one pruning boundary (Sec. 3; eq. problem; Algorithm 1
+ * phase 3) as one call on one stream: stepkv_score (stepkv_score_from_lse
+ * when lse_win is non-NULL), then stepkv_select, then stepkv_compact, with
+ * the same arguments, layouts and results as those calls.
+ *   scores  fp32 [L][Hkv][Ntot] or NULL (kept in the workspace)
+ *   idx     int32 [L][Hkv][Ntot] or NULL (kept in the workspace)
+ *   cu_retained int32 [S+1] (required)
+ *   k_out, v_out bf16 [L][Hkv][out_rows][d]; out_rows from
+ *           stepkv_retained_rows. A smaller out_rows drops the rows past it
+ *           and sets STEPKV_FLAG_OUT_ROWS in pb->status (when set).
+ * budget / budgets as stepkv_select (budgets: device int32 [S] or NULL).
+ * Errors: those of the three calls (validated before anything is launched),
+ * EWORKSPACE below stepkv_compress_workspace_bytes or misaligned. */
+int stepkv_compress(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                    const void* k, const void* v, const float* lse_win, const int32_t* step_ids,
+                    const uint8_t* protected_mask, const float* step_utility, int32_t budget,
+                    const int32_t* budgets, float* scores, int32_t* idx, int32_t* cu_retained,
+                    int32_t out_rows, void* k_out, void* v_out, void* workspace,
+                    size_t ws_bytes, void* stream);
 
 /* Bytes of device workspace stepkv_decode_attention needs (0 when invalid). */
 size_t stepkv_decode_workspace_bytes(const stepkv_problem* pb, int32_t out_rows);
@@ -366,7 +437,9 @@ size_t stepkv_decode_workspace_bytes(const stepkv_problem* pb, int32_t out_rows)
  * (KV head hq / G), out = softmax(scale * q . K_hat^T) V_hat over the R_s
  * rows of s (R_s from cu_retained, within out_rows). q_dec bf16 [L][S][Hq][d];
  * out fp32 [L][S][Hq][d] (zero for a sequence with no row); scale <= 0
- * selects 1/sqrt(d). Each KV head's rows are read once for its whole query
+ * selects 1/sqrt(d); k_hat and v_hat may be NULL when out_rows is 0. Rows at
+ * or past out_rows are not read (STEPKV_FLAG_OUT_ROWS in pb->status when
+ * cu_retained[S] exceeds out_rows). Each KV head's rows are read once for its whole query
  * group, split over workgroups of 512 rows. Errors: EINVAL, EUNSUPPORTED
  * (d), EWORKSPACE (below stepkv_decode_workspace_bytes, or not 256-byte
  * aligned), EHIP. */

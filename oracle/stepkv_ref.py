@@ -68,6 +68,7 @@ __all__ = [
     "normalised_saliency",
     "priority",
     "select_retained",
+    "retained_count",
     "kept_per_step",
     "step_statistics",
     "compact",
@@ -279,6 +280,12 @@ def select_retained(P: np.ndarray, prunable: np.ndarray, budget: int) -> np.ndar
     keep[~prunable] = True
     keep[take] = True
     return pos[keep]
+
+
+def retained_count(n_tokens: int, n_protected: int, budget: int) -> int:
+    """eq. problem with the Algorithm 1 output size: every protected token plus
+    min(B, N_pr) prunable ones, R = P + min(B, N - P)."""
+    return int(n_protected) + min(int(budget), int(n_tokens) - int(n_protected))
 
 
 def kept_per_step(idx: np.ndarray, step_ids: np.ndarray, prunable: np.ndarray,

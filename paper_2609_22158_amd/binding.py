@@ -16,6 +16,7 @@ import numpy as np
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstepkv.so")
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
+FLAG_STEP_ID, FLAG_NONFINITE, FLAG_OUT_ROWS = 1, 2, 4  # STEPKV_FLAG_*
 CUE_CAP = 64  # STEPKV_CUE_CAP
 MAX_WINDOW_ROWS = 256
 MAX_POOL_KERNEL = 63
@@ -39,6 +40,7 @@ class ProblemC(ctypes.Structure):
         ("cu_seqlens", _vp),
         ("cu_steps_host", _i32p),
         ("cu_steps", _vp),
+        ("status", _vp),
     ]
 
 
@@ -91,6 +93,14 @@ _SIGNATURES = {
     "stepkv_text_cues": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_int64,
                                         ctypes.POINTER(ctypes.c_uint64),
                                         ctypes.POINTER(ctypes.c_int32)]),
+    "stepkv_retained_rows": (ctypes.c_int, [ctypes.POINTER(ProblemC), _vp, ctypes.c_int32, _vp,
+                                            _vp]),
+    "stepkv_status_read": (ctypes.c_int, [ctypes.POINTER(ProblemC),
+                                          ctypes.POINTER(ctypes.c_uint32), ctypes.c_int32, _vp]),
+    "stepkv_compress_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
+    "stepkv_compress": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp, _vp,
+                                       _vp, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp,
+                                       _vp, ctypes.c_int32, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     "stepkv_score_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
     "stepkv_saliency_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
     "stepkv_saliency": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp,
@@ -338,7 +348,7 @@ class Problem:
     """Shape of one compression problem with host and device offset arrays."""
 
     def __init__(self, num_layers: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
-                 window: int, cu_seqlens, cu_steps, device="cuda"):
+                 window: int, cu_seqlens, cu_steps, device="cuda", status: bool = True):
         import torch
 
         self.cu_seqlens = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
@@ -349,9 +359,24 @@ class Problem:
         self.num_layers, self.num_q_heads, self.num_kv_heads = num_layers, num_q_heads, num_kv_heads
         self.head_dim, self.window = head_dim, window
         self.device = device
+        # the device status word the kernels report conditions into (STEPKV_FLAG_*)
+        self.status_dev = torch.zeros(1, dtype=torch.int32, device=device) if status else None
         self.c = ProblemC(num_layers, num_q_heads, num_kv_heads, head_dim, window, self.num_seqs,
                           self.cu_seqlens.ctypes.data_as(_i32p), self.cu_seqlens_dev.data_ptr(),
-                          self.cu_steps.ctypes.data_as(_i32p), self.cu_steps_dev.data_ptr())
+                          self.cu_steps.ctypes.data_as(_i32p), self.cu_steps_dev.data_ptr(),
+                          self.status_dev.data_ptr() if status else None)
+
+    def status(self, clear: bool = False, stream=None) -> int:
+        """stepkv_status_read: the STEPKV_FLAG_* bits reported so far (waits for the stream)."""
+        flags = ctypes.c_uint32(0)
+        _check("stepkv_status_read", load().stepkv_status_read(
+            ctypes.byref(self.c), ctypes.byref(flags), int(bool(clear)), _stream(stream)))
+        return int(flags.value)
+
+    def retained_rows(self, protected, budget: int, budgets=None) -> np.ndarray:
+        """stepkv_retained_rows: cu_retained [S+1] (host int32) for a host protected mask;
+        its last entry is the out_rows that compaction needs."""
+        return retained_rows(self, protected, budget, budgets)
 
     @classmethod
     def from_workload(cls, w, device="cuda") -> "Problem":
@@ -706,19 +731,70 @@ def decode_attention(pb: Problem, q_dec, k_hat, v_hat, cu_retained, out_rows: in
     return out
 
 
-def retained_rows(seqlens: Sequence[int], protected_counts: Sequence[int], budget: int) -> int:
-    """Rows per (layer, head) of the compacted cache: sum of P_s + min(B, N_s - P_s)."""
-    return int(sum(p + min(budget, n - p) for n, p in zip(seqlens, protected_counts)))
+def retained_rows(pb: Problem, protected, budget: int, budgets=None) -> np.ndarray:
+    """stepkv_retained_rows (host): cu_retained [S+1] int32 of the compacted cache, from the
+    host protected mask uint8 [Ntot] and the budget (or per-sequence budgets [S])."""
+    prot = np.ascontiguousarray(protected, dtype=np.uint8)
+    if prot.shape != (pb.ntot,):
+        raise ValueError(f"protected: shape {prot.shape}, expected ({pb.ntot},)")
+    bud = None if budgets is None else np.ascontiguousarray(budgets, dtype=np.int32)
+    if bud is not None and bud.shape != (pb.num_seqs,):
+        raise ValueError(f"budgets: shape {bud.shape}, expected ({pb.num_seqs},)")
+    cu = np.zeros(pb.num_seqs + 1, np.int32)
+    rc = load().stepkv_retained_rows(ctypes.byref(pb.c), prot.ctypes.data, int(budget),
+                                     bud.ctypes.data if bud is not None else None, cu.ctypes.data)
+    _check("stepkv_retained_rows", rc)
+    return cu
 
 
 def compress(pb: Problem, q_win, k, v, step_ids, protected, step_utility, budget: int,
-             out_rows: int, params: Optional[Params] = None, stream=None):
-    """score -> select -> compact on one stream."""
-    sc = score(pb, q_win, k, step_ids, protected, step_utility, params, stream=stream)
-    idx, cu_ret, _ = select(pb, sc["scores"], protected, step_ids, budget, stream=stream)
-    k_hat, v_hat = compact(pb, k, v, idx, cu_ret, out_rows, stream=stream)
-    return {"scores": sc["scores"], "idx": idx, "cu_retained": cu_ret, "k_hat": k_hat,
-            "v_hat": v_hat}
+             out_rows: int, params: Optional[Params] = None, *, lse=None, budgets=None,
+             scores=None, idx=None, cu_retained=None, k_out=None, v_out=None, workspace=None,
+             stream=None):
+    """stepkv_compress: score -> select -> compact in one library call on one stream.
+
+    Returns scores [L][Hkv][Ntot], idx [L][Hkv][Ntot], cu_retained [S+1] and the compacted
+    k_hat / v_hat [L][Hkv][out_rows][d]. With `lse` the saliency takes one sweep."""
+    import torch
+
+    lib = load()
+    L, Hkv, d, W, S, dev = (pb.num_layers, pb.num_kv_heads, pb.head_dim, pb.window, pb.num_seqs,
+                            pb.device)
+    qp = _need(q_win, torch.bfloat16, (L, S, W, pb.num_q_heads, d), "q_win")
+    kp = _need(k, torch.bfloat16, (L, Hkv, pb.ntot, d), "k")
+    vp = _need(v, torch.bfloat16, (L, Hkv, pb.ntot, d), "v")
+    lp = _need(lse, torch.float32, (L, S, W, pb.num_q_heads), "lse") if lse is not None else None
+    sp = _need(step_ids, torch.int32, (pb.ntot,), "step_ids")
+    pp = _need(protected, torch.uint8, (pb.ntot,), "protected")
+    up = _need(step_utility, torch.float32, (pb.total_steps,), "step_utility")
+    bp = _need(budgets, torch.int32, (S,), "budgets") if budgets is not None else None
+    if scores is None:
+        scores = torch.empty((L, Hkv, pb.ntot), dtype=torch.float32, device=dev)
+    if idx is None:
+        idx = torch.empty((L, Hkv, pb.ntot), dtype=torch.int32, device=dev)
+    if cu_retained is None:
+        cu_retained = torch.empty(S + 1, dtype=torch.int32, device=dev)
+    if k_out is None:
+        k_out = torch.empty((L, Hkv, out_rows, d), dtype=torch.bfloat16, device=dev)
+    if v_out is None:
+        v_out = torch.empty((L, Hkv, out_rows, d), dtype=torch.bfloat16, device=dev)
+    for t, dt, shape, name in ((scores, torch.float32, (L, Hkv, pb.ntot), "scores"),
+                               (idx, torch.int32, (L, Hkv, pb.ntot), "idx"),
+                               (cu_retained, torch.int32, (S + 1,), "cu_retained"),
+                               (k_out, torch.bfloat16, (L, Hkv, out_rows, d), "k_out"),
+                               (v_out, torch.bfloat16, (L, Hkv, out_rows, d), "v_out")):
+        _need(t, dt, shape, name)
+    if workspace is None:
+        need = int(lib.stepkv_compress_workspace_bytes(ctypes.byref(pb.c)))
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lib.stepkv_compress(ctypes.byref(pb.c), ctypes.byref((params or Params()).c()), qp, kp,
+                             vp, lp, sp, pp, up, int(budget), bp, scores.data_ptr(),
+                             idx.data_ptr(), cu_retained.data_ptr(), int(out_rows),
+                             k_out.data_ptr(), v_out.data_ptr(), workspace.data_ptr(),
+                             workspace.numel(), _stream(stream))
+    _check("stepkv_compress", rc)
+    return {"scores": scores, "idx": idx, "cu_retained": cu_retained, "k_hat": k_out,
+            "v_hat": v_out}
 
 
 def bf16_from_bits(bits: np.ndarray, device="cuda"):

@@ -162,6 +162,43 @@ int64_t stepkv_budget_from_ratio(double rho, int64_t n_prunable) {
   return std::max<int64_t>(1, b);
 }
 
+int stepkv_retained_rows(const stepkv_problem* pb, const uint8_t* protected_host, int32_t budget,
+                         const int32_t* budgets_host, int32_t* cu_retained_host) {
+  if (!pb || pb->num_seqs < 1 || !pb->cu_seqlens_host || !protected_host || !cu_retained_host)
+    return STEPKV_EINVAL;
+  if (!monotone_from_zero(pb->cu_seqlens_host, pb->num_seqs)) return STEPKV_EINVAL;
+  if (!budgets_host && budget < 1) return STEPKV_EINVAL;
+  int64_t acc = 0;
+  cu_retained_host[0] = 0;
+  for (int s = 0; s < pb->num_seqs; ++s) {
+    const int32_t a = pb->cu_seqlens_host[s], b = pb->cu_seqlens_host[s + 1];
+    int64_t n_prot = 0;
+    for (int32_t i = a; i < b; ++i) n_prot += protected_host[i] != 0;
+    const int64_t n_pr = (b - a) - n_prot;
+    const int64_t B = budgets_host ? std::max<int32_t>(1, budgets_host[s]) : budget;
+    acc += n_prot + std::min(B, n_pr);
+    if (acc > std::numeric_limits<int32_t>::max()) return STEPKV_EINVAL;
+    cu_retained_host[s + 1] = (int32_t)acc;
+  }
+  return STEPKV_OK;
+}
+
+int stepkv_status_read(const stepkv_problem* pb, uint32_t* flags_host, int32_t clear,
+                       void* stream) {
+  if (!pb || !pb->status || !flags_host) return STEPKV_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint32_t v = 0u;
+  if (hipMemcpyAsync(&v, pb->status, sizeof(v), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return STEPKV_EHIP;
+  if (clear) {
+    if (launch_fill_u32(pb->status, 0u, 1, st) != hipSuccess || hipStreamSynchronize(st) != hipSuccess)
+      return STEPKV_EHIP;
+  }
+  *flags_host = v;
+  return STEPKV_OK;
+}
+
 int stepkv_step_update(stepkv_step_state* st, float valid, float gain, float red,
                        const float* obs_sim_prev, const stepkv_params* prm, float* S_out) {
   if (!st || !prm || !S_out || !st->r || !st->c) return STEPKV_EINVAL;
@@ -263,6 +300,7 @@ int run_priority(const stepkv_problem* pb, const stepkv_params* prm, const float
   fa.util = util;
   fa.scores = scores;
   fa.stats = stats;
+  fa.status = pb->status;
   fa.S = pb->num_seqs;
   fa.LH = pb->num_layers * pb->num_kv_heads;
   fa.ntot = pb->cu_seqlens_host[pb->num_seqs];
@@ -320,6 +358,22 @@ SharedLayout shared_layout(const stepkv_problem* pb, int n) {
   w.cmax = align_up(w.shared + sizeof(float) * ntot);
   w.total = align_up(w.cmax + sizeof(float) * shared_chunks(pb->cu_seqlens_host, pb->num_seqs));
   return w;
+}
+
+// stepkv_compress: the score workspace (saliency buffer included), then the
+// scores and the retained positions for callers that do not keep them.
+struct CompressLayout {
+  size_t scores, idx, total;
+};
+
+CompressLayout compress_layout(const stepkv_problem* pb) {
+  const size_t entries = (size_t)pb->num_layers * pb->num_kv_heads *
+                         (size_t)pb->cu_seqlens_host[pb->num_seqs];
+  CompressLayout c;
+  c.scores = layout(pb, plan_saliency(pb)).total;
+  c.idx = align_up(c.scores + sizeof(float) * entries);
+  c.total = align_up(c.idx + sizeof(int32_t) * entries);
+  return c;
 }
 
 }  // namespace
@@ -477,6 +531,7 @@ int stepkv_score_shared(const stepkv_problem* pb, const stepkv_params* prm, cons
     sa.prot = protected_mask;
     sa.util = step_utility;
     sa.scores = scores;
+    sa.status = pb->status;
     sa.S = pb->num_seqs;
     sa.ntot = ntot;
     sa.nheads = n * pb->num_kv_heads;
@@ -509,7 +564,8 @@ int stepkv_compact_shared(const stepkv_problem* pb, const void* k, const void* v
                           void* k_out, void* v_out, void* stream) {
   const int rc = check_problem(pb);
   if (rc != STEPKV_OK) return rc;
-  if (!k || !v || !idx || !cu_retained || !k_out || !v_out || out_rows < 0) return STEPKV_EINVAL;
+  if (!k || !v || !idx || !cu_retained || out_rows < 0) return STEPKV_EINVAL;
+  if (out_rows > 0 && (!k_out || !v_out)) return STEPKV_EINVAL;  // NULL outputs hold 0 rows
   CompactArgs a;
   a.k = static_cast<const uint16_t*>(k);
   a.v = static_cast<const uint16_t*>(v);
@@ -524,6 +580,7 @@ int stepkv_compact_shared(const stepkv_problem* pb, const void* k, const void* v
   a.out_rows = out_rows;
   a.d = pb->head_dim;
   a.shared_idx = 1;
+  a.status = pb->status;
   return hip_status(launch_compact(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -559,7 +616,8 @@ int stepkv_compact(const stepkv_problem* pb, const void* k, const void* v, const
                    void* stream) {
   const int rc = check_problem(pb);
   if (rc != STEPKV_OK) return rc;
-  if (!k || !v || !idx || !cu_retained || !k_out || !v_out || out_rows < 0) return STEPKV_EINVAL;
+  if (!k || !v || !idx || !cu_retained || out_rows < 0) return STEPKV_EINVAL;
+  if (out_rows > 0 && (!k_out || !v_out)) return STEPKV_EINVAL;  // NULL outputs hold 0 rows
   CompactArgs a;
   a.k = static_cast<const uint16_t*>(k);
   a.v = static_cast<const uint16_t*>(v);
@@ -574,7 +632,48 @@ int stepkv_compact(const stepkv_problem* pb, const void* k, const void* v, const
   a.out_rows = out_rows;
   a.d = pb->head_dim;
   a.shared_idx = 0;
+  a.status = pb->status;
   return hip_status(launch_compact(a, static_cast<hipStream_t>(stream)));
+}
+
+size_t stepkv_compress_workspace_bytes(const stepkv_problem* pb) {
+  if (check_problem(pb) != STEPKV_OK) return 0;
+  return compress_layout(pb).total;
+}
+
+int stepkv_compress(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                    const void* k, const void* v, const float* lse_win, const int32_t* step_ids,
+                    const uint8_t* protected_mask, const float* step_utility, int32_t budget,
+                    const int32_t* budgets, float* scores, int32_t* idx, int32_t* cu_retained,
+                    int32_t out_rows, void* k_out, void* v_out, void* workspace,
+                    size_t ws_bytes, void* stream) {
+  // every argument of the three steps is validated before anything is launched
+  int rc = check_problem(pb);
+  if (rc == STEPKV_OK) rc = check_params(pb, prm);
+  if (rc != STEPKV_OK) return rc;
+  if (!q_win || !k || !v || !step_ids || !protected_mask || !cu_retained || out_rows < 0)
+    return STEPKV_EINVAL;
+  if (out_rows > 0 && (!k_out || !v_out)) return STEPKV_EINVAL;  // NULL outputs hold 0 rows
+  if (!step_utility && pb->cu_steps_host[pb->num_seqs] > 0) return STEPKV_EINVAL;
+  if (!budgets && budget < 1) return STEPKV_EINVAL;
+  const CompressLayout cl = compress_layout(pb);
+  if (!workspace || ws_bytes < cl.total || !aligned(workspace)) return STEPKV_EWORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  float* P = scores ? scores : reinterpret_cast<float*>(ws + cl.scores);
+  int32_t* I = idx ? idx : reinterpret_cast<int32_t*>(ws + cl.idx);
+  if (pb->cu_seqlens_host[pb->num_seqs] > 0) {
+    float* sal = reinterpret_cast<float*>(ws + layout(pb, plan_saliency(pb)).sal);
+    rc = run_saliency(pb, prm, q_win, k, sal, ws, st,
+                      lse_win ? SaliencyMode::kFromLse : SaliencyMode::kBoth, lse_win);
+    if (rc == STEPKV_OK)
+      rc = run_priority(pb, prm, sal, step_ids, protected_mask, step_utility, P, nullptr, st);
+    if (rc != STEPKV_OK) return rc;
+  }
+  rc = stepkv_select(pb, P, protected_mask, step_ids, budget, budgets, I, cu_retained, nullptr,
+                     stream);
+  if (rc != STEPKV_OK) return rc;
+  return stepkv_compact(pb, k, v, I, cu_retained, out_rows, k_out, v_out, stream);
 }
 
 size_t stepkv_decode_workspace_bytes(const stepkv_problem* pb, int32_t out_rows) {
@@ -594,8 +693,9 @@ int stepkv_decode_attention(const stepkv_problem* pb, const void* q_dec, const v
                             void* stream) {
   const int rc = check_problem(pb);
   if (rc != STEPKV_OK) return rc;
-  if (!q_dec || !k_hat || !v_hat || !cu_retained || !out || out_rows < 0 || !std::isfinite(scale))
+  if (!q_dec || !cu_retained || !out || out_rows < 0 || !std::isfinite(scale))
     return STEPKV_EINVAL;
+  if (out_rows > 0 && (!k_hat || !v_hat)) return STEPKV_EINVAL;  // NULL caches hold 0 rows
   if (!workspace || ws_bytes < stepkv_decode_workspace_bytes(pb, out_rows) || !aligned(workspace))
     return STEPKV_EWORKSPACE;
   DecodeArgs a;
@@ -606,6 +706,7 @@ int stepkv_decode_attention(const stepkv_problem* pb, const void* q_dec, const v
   a.out = out;
   a.cu_seqlens = pb->cu_seqlens;
   a.partial = static_cast<float*>(workspace);
+  a.status = pb->status;
   a.L = pb->num_layers;
   a.S = pb->num_seqs;
   a.Hq = pb->num_q_heads;

@@ -40,6 +40,21 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi(hi, __builtin_amdgcn_mbcnt_lo(lo, 0u));
 }
 
+// ORs the STEPKV_FLAG_* bits that any lane of the wave met into the device
+// status word (one atomic per wave, none when no lane met a condition). Every
+// lane of the wave must reach the call.
+__device__ __forceinline__ void report_flags(uint32_t* status, uint32_t bits) {
+  if (status == nullptr) return;
+  uint32_t w = 0u;
+#pragma unroll
+  for (uint32_t b = 1u; b <= 4u; b <<= 1) w |= __ballot((bits & b) != 0u) ? b : 0u;
+  if (w != 0u && (threadIdx.x & (kWave - 1)) == __builtin_ctzll(__ballot(1)))
+    atomicOr(status, w);
+}
+
+// x is neither NaN nor infinite.
+__device__ __forceinline__ bool finite(float x) { return fabsf(x) <= 3.40282347e38f; }
+
 // 2^x on the transcendental unit (v_exp_f32); -inf gives 0.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 

@@ -38,6 +38,8 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   const int bid = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
   if (bid >= a.LH * nb) return;
   const int lh = bid / nb, rb = bid - lh * nb;
+  if (bid == 0 && threadIdx.x == 0 && a.status && a.cu_retained[a.S] > a.out_rows)
+    atomicOr(a.status, kFlagOutRows);  // the rows past out_rows are dropped
   const int total = min(a.out_rows, a.cu_retained[a.S]);
   const int sub = threadIdx.x / kLanesPerRow, piece = threadIdx.x % kLanesPerRow;
   const size_t in_head = (size_t)lh * a.ntot;
@@ -86,11 +88,32 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   }
 }
 
+__global__ void out_rows_check_kernel(const int32_t* __restrict__ cu_retained, int S,
+                                      int out_rows, uint32_t* status) {
+  if (threadIdx.x == 0 && cu_retained[S] > out_rows) atomicOr(status, kFlagOutRows);
+}
+
+__global__ void fill_u32_kernel(uint32_t* __restrict__ p, uint32_t v, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
 }  // namespace
+
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_u32_kernel, dim3((n + 255) / 256), dim3(256), 0, st, p, v, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st) {
   // no tokens: nothing to gather (and no row 0 for skipped rows to stand on)
-  if (a.out_rows <= 0 || a.LH == 0 || a.ntot == 0) return hipSuccess;
+  if (a.out_rows <= 0 || a.LH == 0 || a.ntot == 0) {
+    if (a.status && a.LH > 0)  // rows may still be needed past out_rows = 0
+      hipLaunchKernelGGL(out_rows_check_kernel, dim3(1), dim3(64), 0, st, a.cu_retained, a.S,
+                         a.out_rows, a.status);
+    return hipGetLastError();
+  }
   auto grid = [&](int rows_per_block) {  // a multiple of 8: one eighth per XCD
     const unsigned nb = (unsigned)((a.out_rows + rows_per_block - 1) / rows_per_block);
     return dim3(((unsigned)a.LH * nb + 7u) / 8u * 8u);

@@ -39,6 +39,8 @@ __global__ __launch_bounds__(kThreads) void decode_simple_kernel(DecodeArgs a) {
   const int s = (blockIdx.x / a.Hq) % a.S;
   const int l = blockIdx.x / (a.Hq * a.S);
   const int lh = l * a.Hkv + hq / a.G;
+  if (blockIdx.x == 0 && tid == 0 && a.status && a.cu_retained[a.S] > a.out_rows)
+    atomicOr(a.status, kFlagOutRows);  // rows past out_rows are not read
   const int r0 = a.cu_retained[s];
   const int r1 = min(a.cu_retained[s + 1], a.out_rows);
   const int R = max(0, r1 - r0);
@@ -338,6 +340,8 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(DecodeArgs a) {
   const int l = blockIdx.x / (a.Hq * a.S);
   const int lh = l * a.Hkv + hq / a.G, g = hq % a.G;
   const int dd = threadIdx.x;
+  if (blockIdx.x == 0 && dd == 0 && a.status && a.cu_retained[a.S] > a.out_rows)
+    atomicOr(a.status, kFlagOutRows);  // the split kernel read no row past out_rows
   int first = 0;  // global splits of the sequences before s (every lane adds them all)
   for (int s2 = 0; s2 < s; ++s2) first += splits_of(a, s2);
   const int last = first + splits_of(a, s);

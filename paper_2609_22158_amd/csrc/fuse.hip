@@ -115,9 +115,11 @@ __global__ __launch_bounds__(kThreads) void fuse_batched_kernel(FuseArgs a) {
       pb[j] = prot[ic];
     }
   }
+  uint32_t bad = 0u;  // STEPKV_FLAG_* conditions met by this thread
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     const bool pr = ns > 0 && tid + kThreads * j < ns && pb[j] == 0;
+    bad |= pr && !finite(x[j]) ? kFlagNonFinite : 0u;
     x[j] = pr ? x[j] : 0.f;
     pb[j] = pr ? 1u : 0u;
   }
@@ -202,6 +204,7 @@ __global__ __launch_bounds__(kThreads) void fuse_batched_kernel(FuseArgs a) {
         const bool ok = pr && kk >= 0 && kk < nsteps;
         const float th = u[b][r] * inv;
         const float util = ok ? tabs.util[ok ? kk : 0] : 0.f;
+        bad |= (pr && !ok ? kFlagStepId : 0u) | (!finite(util) ? kFlagNonFinite : 0u);
         pv[r] = pr ? fmaf(a.alpha, th, a.beta * util) : -INFINITY;
         if (stats) {
           const int key = ok ? kk : -1;
@@ -233,6 +236,7 @@ __global__ __launch_bounds__(kThreads) void fuse_batched_kernel(FuseArgs a) {
       __syncthreads();  // the next batch reuses the stage
     }
   }
+  report_flags(a.status, bad);
   if (stats) {
     __syncthreads();
     write_stats(a, tabs, lh, st0, nsteps);
@@ -292,6 +296,7 @@ __global__ __launch_bounds__(kThreads) void fuse_stream_kernel(FuseArgs a) {
   for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wred[w]);
   const float inv = M > 0.f ? 1.0f / M : 0.f;
   float* __restrict__ out = a.scores + (size_t)lh * a.ntot + seq0;
+  uint32_t bad = 0u;  // STEPKV_FLAG_* conditions met by this thread
   for (int base = 0; base < ns; base += kThreads) {
     const float uu = pooled(base);
     const int i = base + tid;
@@ -302,7 +307,11 @@ __global__ __launch_bounds__(kThreads) void fuse_stream_kernel(FuseArgs a) {
       kk = sid[i];
       const bool ok = pr && kk >= 0 && kk < nsteps;
       th = uu * inv;
-      out[i] = pr ? fmaf(a.alpha, th, a.beta * (ok ? tabs.util[kk] : 0.f)) : -INFINITY;
+      const float util = ok ? tabs.util[kk] : 0.f;
+      // a non-finite prunable saliency makes every pooled value around it non-finite
+      bad |= (pr && !ok ? kFlagStepId : 0u) |
+             (pr && !(finite(uu) && finite(util)) ? kFlagNonFinite : 0u);
+      out[i] = pr ? fmaf(a.alpha, th, a.beta * util) : -INFINITY;
       if (!ok) kk = -1;
     }
     if (stats) {
@@ -320,6 +329,7 @@ __global__ __launch_bounds__(kThreads) void fuse_stream_kernel(FuseArgs a) {
       }
     }
   }
+  report_flags(a.status, bad);
   if (stats) {
     __syncthreads();
     write_stats(a, tabs, lh, st0, nsteps);
@@ -458,16 +468,20 @@ __global__ __launch_bounds__(kShChunk) void shared_fuse_kernel(SharedPrioArgs a)
   for (int w = 0; w < kShChunk / kWave; ++w) M = fmaxf(M, wred[w]);
   const float inv = M > 0.f ? 1.0f / M : 0.f;
   const int p = p0 + (int)threadIdx.x;
-  if (p >= ns) return;
-  float u = 0.f;
-  for (int o = 0; o <= 2 * a.half; ++o) u += am[threadIdx.x + o];
-  const int i = seq0 + p;
-  const bool pr = a.prot[i] == 0;
-  const int st0 = a.cu_steps[s], nsteps = a.cu_steps[s + 1] - st0;
-  const int kk = a.step_ids[i];
-  const bool ok = pr && kk >= 0 && kk < nsteps;
-  const float util = ok ? a.util[st0 + kk] : 0.f;
-  a.scores[i] = pr ? fmaf(a.alpha, u * inv, a.beta * util) : -INFINITY;
+  uint32_t bad = 0u;
+  if (p < ns) {
+    float u = 0.f;
+    for (int o = 0; o <= 2 * a.half; ++o) u += am[threadIdx.x + o];
+    const int i = seq0 + p;
+    const bool pr = a.prot[i] == 0;
+    const int st0 = a.cu_steps[s], nsteps = a.cu_steps[s + 1] - st0;
+    const int kk = a.step_ids[i];
+    const bool ok = pr && kk >= 0 && kk < nsteps;
+    const float util = ok ? a.util[st0 + kk] : 0.f;
+    bad = (pr && !ok ? kFlagStepId : 0u) | (pr && !(finite(u) && finite(util)) ? kFlagNonFinite : 0u);
+    a.scores[i] = pr ? fmaf(a.alpha, u * inv, a.beta * util) : -INFINITY;
+  }
+  report_flags(a.status, bad);
 }
 
 }  // namespace

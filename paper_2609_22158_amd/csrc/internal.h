@@ -45,6 +45,7 @@ struct FuseArgs {
   const float* util;         // [cu_steps[S]]
   float* scores;             // [L*Hkv][Ntot]
   void* stats;               // stepkv_step_stat [L*Hkv][cu_steps[S]] or null
+  uint32_t* status;          // device status word (STEPKV_FLAG_*) or null
   int S, LH, ntot, total_steps, half, max_steps, max_len;
   float alpha, beta;
 };
@@ -61,6 +62,7 @@ struct SharedPrioArgs {
   const uint8_t* prot;       // [Ntot]
   const float* util;         // [cu_steps[S]]
   float* scores;             // [Ntot]
+  uint32_t* status;          // device status word (STEPKV_FLAG_*) or null
   int S, ntot, nheads, half;
   float alpha, beta;
 };
@@ -93,10 +95,18 @@ struct CompactArgs {
   const int32_t* cu_retained;// [S+1]
   uint16_t* k_out;           // bf16 [L*Hkv][out_rows][d]
   uint16_t* v_out;
+  uint32_t* status;          // device status word (STEPKV_FLAG_*) or null
   int S, LH, ntot, out_rows, d;
   int shared_idx;            // nonzero: one idx row for every (layer, KV head)
 };
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
+
+// p[0 .. n) = v on the stream (a kernel, not a memset, so that it can sit in
+// a captured graph).
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int n, hipStream_t st);
+
+// Device status bits (the STEPKV_FLAG_* values of stepkv.h).
+constexpr uint32_t kFlagStepId = 1u, kFlagNonFinite = 2u, kFlagOutRows = 4u;
 
 // ---------------------------------------------------------------- decode check
 struct DecodeArgs {
@@ -107,6 +117,7 @@ struct DecodeArgs {
   float* out;                // [L][S][Hq][d]
   const int32_t* cu_seqlens; // [S+1]
   float* partial;            // workspace: [L*Hkv][total_splits][G][d+2] (o, m, z)
+  uint32_t* status;          // device status word (STEPKV_FLAG_*) or null
   int L, S, Hq, Hkv, G, d, out_rows, total_splits;
   float scale;
 };

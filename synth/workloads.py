@@ -157,11 +157,6 @@ class Workload:
     def total_steps(self) -> int:
         return int(self.cu_steps[-1])
 
-    def retained_rows(self, budget: Optional[int] = None) -> List[int]:
-        """Rows kept per sequence and head: protected + min(B, prunable)."""
-        b = self.budget if budget is None else budget
-        return [p + min(b, n - p) for n, p in zip(self.seqlens, self.protected_len)]
-
 
 # ------------------------------------------------------------ step spans
 def _integerise(x: np.ndarray, total: int, cap: Optional[int] = None) -> np.ndarray:

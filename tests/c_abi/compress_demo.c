@@ -10,7 +10,10 @@
  *  - protected tokens score -inf and prunable ones a finite P >= 0;
  *  - cu_retained[s+1] - cu_retained[s] = n_protected + min(B, N - n_protected)
  *    and each retained position list is ascending and holds the prefix;
- *  - every compacted K and V row equals the source row it names (bit-exact).
+ *  - every compacted K and V row equals the source row it names (bit-exact);
+ *  - stepkv_retained_rows on the host gives the selection's cu_retained,
+ *    stepkv_compress gives the three calls' outputs bit for bit, and the
+ *    device status word stays clear.
  * Prints "ok" and returns 0, or names the first failed check and returns 1.
  */
 #include <hip/hip_runtime_api.h>
@@ -96,7 +99,10 @@ int main(void) {
   HIP(hipMemcpy(dcu, cu, sizeof cu, hipMemcpyHostToDevice));
   HIP(hipMemcpy(dcus, cu_steps, sizeof cu_steps, hipMemcpyHostToDevice));
 
-  stepkv_problem pb = {L, HQ, HKV, D, W, S, cu, dcu, cu_steps, dcus};
+  void* dstatus;
+  HIP(hipMalloc(&dstatus, sizeof(uint32_t)));
+  HIP(hipMemset(dstatus, 0, sizeof(uint32_t)));
+  stepkv_problem pb = {L, HQ, HKV, D, W, S, cu, dcu, cu_steps, dcus, (uint32_t*)dstatus};
   stepkv_params prm;
   stepkv_params_default(&prm);
   const size_t ws = stepkv_score_workspace_bytes(&pb);
@@ -107,11 +113,9 @@ int main(void) {
   HIP(hipMalloc(&dws, ws));
   STEPKV(stepkv_score(&pb, &prm, dq, dk, dsid, dprot, dutil, dscores, dsal, NULL, dws, ws, NULL));
 
-  int32_t out_rows = 0;
-  for (int s = 0; s < S; ++s) {
-    const int n_pr = kLens[s] - PROT;
-    out_rows += PROT + (BUDGET < n_pr ? BUDGET : n_pr);
-  }
+  int32_t cu_host[S + 1];
+  STEPKV(stepkv_retained_rows(&pb, prot, BUDGET, NULL, cu_host));
+  const int32_t out_rows = cu_host[S];
   const size_t nout = (size_t)L * HKV * out_rows * D;
   void *dko, *dvo;
   HIP(hipMalloc(&didx, sizeof(int32_t) * nrow));
@@ -120,7 +124,20 @@ int main(void) {
   HIP(hipMalloc(&dvo, nout * 2));
   STEPKV(stepkv_select(&pb, dscores, dprot, dsid, BUDGET, NULL, didx, dcur, NULL, NULL));
   STEPKV(stepkv_compact(&pb, dk, dv, didx, dcur, out_rows, dko, dvo, NULL));
+  /* the same pass as one call, its scores and positions kept in its workspace */
+  const size_t cws = stepkv_compress_workspace_bytes(&pb);
+  CHECK(cws >= ws, "compress workspace size");
+  void *dcws, *dcur2, *dko2, *dvo2;
+  HIP(hipMalloc(&dcws, cws));
+  HIP(hipMalloc(&dcur2, sizeof cu));
+  HIP(hipMalloc(&dko2, nout * 2));
+  HIP(hipMalloc(&dvo2, nout * 2));
+  STEPKV(stepkv_compress(&pb, &prm, dq, dk, dv, NULL, dsid, dprot, dutil, BUDGET, NULL, NULL, NULL,
+                         dcur2, out_rows, dko2, dvo2, dcws, cws, NULL));
   HIP(hipDeviceSynchronize());
+  uint32_t flags = 0xffffffffu;
+  STEPKV(stepkv_status_read(&pb, &flags, 1, NULL));
+  CHECK(flags == 0u, "device status 0x%x on clean inputs", flags);
 
   float* sal = malloc(sizeof(float) * nrow);
   float* sc = malloc(sizeof(float) * nrow);
@@ -134,6 +151,20 @@ int main(void) {
   HIP(hipMemcpy(cur, dcur, sizeof cur, hipMemcpyDeviceToHost));
   HIP(hipMemcpy(ko, dko, nout * 2, hipMemcpyDeviceToHost));
   HIP(hipMemcpy(vo, dvo, nout * 2, hipMemcpyDeviceToHost));
+  {
+    int32_t cur2[S + 1];
+    uint16_t* ko2 = malloc(nout * 2);
+    uint16_t* vo2 = malloc(nout * 2);
+    HIP(hipMemcpy(cur2, dcur2, sizeof cur2, hipMemcpyDeviceToHost));
+    HIP(hipMemcpy(ko2, dko2, nout * 2, hipMemcpyDeviceToHost));
+    HIP(hipMemcpy(vo2, dvo2, nout * 2, hipMemcpyDeviceToHost));
+    CHECK(memcmp(cur2, cur, sizeof cur) == 0 && memcmp(cu_host, cur, sizeof cur) == 0,
+          "cu_retained of compress, select and the host rule");
+    CHECK(memcmp(ko2, ko, nout * 2) == 0 && memcmp(vo2, vo, nout * 2) == 0,
+          "compress equals score, select, compact");
+    free(ko2);
+    free(vo2);
+  }
 
   const double rows = (double)W * (HQ / HKV);
   CHECK(cur[0] == 0, "cu_retained[0]");

@@ -40,6 +40,11 @@ def gpu_utilities(w) -> np.ndarray:
     return np.concatenate(out).astype(np.float32) if out else np.zeros(0, np.float32)
 
 
+def ref_rows(w, budget):
+    """The oracle's retained rows per sequence and head."""
+    return [O.retained_count(n, p, budget) for n, p in zip(w.seqlens, w.protected_len)]
+
+
 class HipRun:
     """Device copies of a workload and the HIP path's outputs."""
 
@@ -60,7 +65,7 @@ class HipRun:
         self.prot = torch.from_numpy(w.protected).cuda()
         self.util_host = gpu_utilities(w)
         self.util = torch.from_numpy(self.util_host).cuda()
-        self.out_rows = B.retained_rows(w.seqlens, w.protected_len, self.budget)
+        self.out_rows = int(self.pb.retained_rows(w.protected, self.budget)[-1])
 
     def score(self, **kw):
         return self.B.score(self.pb, self.q, self.k, self.sid, self.prot, self.util, self.params,
@@ -101,20 +106,21 @@ def oracle_lse(w, causal: bool, scale=None) -> np.ndarray:
     return out
 
 
-def run_oracle(w, budget, params, heads=None, want_saliency=True, lse_win=None):
-    """Oracle results keyed by (s, l, h); `heads` restricts it to some (l, h) pairs.
+def run_oracle(w, budget, params, heads=None, want_saliency=True, lse_win=None, seqs=None):
+    """Oracle results keyed by (s, l, h); `heads` restricts it to some (l, h) pairs and
+    `seqs` to some sequences.
 
     lse_win (natural log, [L][S][W][Hq]) takes the saliency from given row LSEs."""
     S = oracle_utilities(w)
     args = (w.q_win, w.k, None, w.cu_seqlens, w.step_ids, w.protected, w.cu_steps, S, budget,
             oracle_params(params))
     if heads is None:
-        res = O.compress(*args, want_saliency=want_saliency, lse_win=lse_win)
+        res = O.compress(*args, want_saliency=want_saliency, lse_win=lse_win, seqs=seqs)
     else:
         res = None
         for l, h in heads:
             part = O.compress(*args, layers=[l], heads=[h], want_saliency=want_saliency,
-                              lse_win=lse_win)
+                              lse_win=lse_win, seqs=seqs)
             if res is None:
                 res = part
             else:

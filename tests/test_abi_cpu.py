@@ -31,7 +31,7 @@ def _declared_functions():
 
 def test_exports_every_declared_function(lib):
     names = _declared_functions()
-    assert len(names) == 24, names
+    assert len(names) == 28, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGNATURES)
@@ -239,3 +239,90 @@ def test_step_tracker_incremental_matches_oracle(lib):
     np.testing.assert_array_equal(out, S)
     with pytest.raises(ValueError):
         tr.update(1.0, 0.5, 0.0, np.zeros(3))  # wrong sim_prev length
+
+
+# ---------------------------------------------------------------- retained rows, compress, status
+@pytest.mark.parametrize("seed", range(5))
+def test_retained_rows_matches_oracle(lib, seed):
+    """stepkv_retained_rows gives the oracle's R_s = P_s + min(B_s, N_s - P_s), prefix-summed,
+    for any protected mask (not only a prefix), with one budget or per-sequence budgets
+    (below 1 taken as 1, as stepkv_select does)."""
+    rng = np.random.default_rng(seed)
+    S = int(rng.integers(1, 7))
+    lens = rng.integers(0, 300, S)
+    lens[rng.integers(0, S)] = 0  # an empty sequence
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    prot = (rng.random(int(cu[-1])) < 0.2).astype(np.uint8)
+    pb = _problem(cu=tuple(cu), cu_steps=tuple(np.arange(S + 1)))
+    budget = int(rng.integers(1, 200))
+    got = np.zeros(S + 1, np.int32)
+    assert lib.stepkv_retained_rows(ctypes.byref(pb), prot.ctypes.data, budget, None,
+                                    got.ctypes.data) == B.OK
+    n_prot = [int(prot[cu[s]:cu[s + 1]].sum()) for s in range(S)]
+    want = np.concatenate([[0], np.cumsum([O.retained_count(int(lens[s]), n_prot[s], budget)
+                                           for s in range(S)])])
+    np.testing.assert_array_equal(got, want)
+    budgets = rng.integers(-3, 200, S).astype(np.int32)
+    assert lib.stepkv_retained_rows(ctypes.byref(pb), prot.ctypes.data, 0, budgets.ctypes.data,
+                                    got.ctypes.data) == B.OK
+    want = np.concatenate([[0], np.cumsum([O.retained_count(int(lens[s]), n_prot[s],
+                                                            max(1, int(budgets[s])))
+                                           for s in range(S)])])
+    np.testing.assert_array_equal(got, want)
+
+
+def test_retained_rows_rejects(lib):
+    pb = _problem()
+    prot = np.zeros(3000, np.uint8)
+    out = np.zeros(3, np.int32)
+    f = lib.stepkv_retained_rows
+    assert f(None, prot.ctypes.data, 4, None, out.ctypes.data) == B.EINVAL
+    assert f(ctypes.byref(pb), None, 4, None, out.ctypes.data) == B.EINVAL
+    assert f(ctypes.byref(pb), prot.ctypes.data, 4, None, None) == B.EINVAL
+    assert f(ctypes.byref(pb), prot.ctypes.data, 0, None, out.ctypes.data) == B.EINVAL
+    assert f(ctypes.byref(_problem(cu=(0, 10, 5))), prot.ctypes.data, 4, None,
+             out.ctypes.data) == B.EINVAL
+    assert f(ctypes.byref(pb), prot.ctypes.data, 4, None, out.ctypes.data) == B.OK
+    assert list(out) == [0, 4, 8]
+
+
+def _compress(lib, pb, ws_bytes=None, **kw):
+    args = dict(prm=B.Params().c(), q=FAKE, k=FAKE, v=FAKE, lse=None, sid=FAKE, prot=FAKE,
+                util=FAKE, budget=4, budgets=None, scores=None, idx=None, cu_ret=FAKE,
+                out_rows=8, k_out=FAKE, v_out=FAKE, ws=FAKE * 16)
+    args.update(kw)
+    need = lib.stepkv_compress_workspace_bytes(ctypes.byref(pb))
+    a = args
+    return lib.stepkv_compress(ctypes.byref(pb), ctypes.byref(a["prm"]), a["q"], a["k"], a["v"],
+                               a["lse"], a["sid"], a["prot"], a["util"], a["budget"],
+                               a["budgets"], a["scores"], a["idx"], a["cu_ret"], a["out_rows"],
+                               a["k_out"], a["v_out"], a["ws"],
+                               need if ws_bytes is None else ws_bytes, None)
+
+
+def test_compress_workspace_and_rejects(lib):
+    """stepkv_compress validates the arguments of all three steps before launching any."""
+    pb = _problem()
+    need = lib.stepkv_compress_workspace_bytes(ctypes.byref(pb))
+    score_ws = lib.stepkv_score_workspace_bytes(ctypes.byref(pb))
+    # the score workspace plus fp32 scores and int32 positions for every entry
+    assert need >= score_ws + 2 * 4 * 2 * 2 * 3000 and need % 256 == 0
+    assert lib.stepkv_compress_workspace_bytes(ctypes.byref(_problem(Hq=7))) == 0
+    for kw in (dict(q=None), dict(k=None), dict(v=None), dict(sid=None), dict(prot=None),
+               dict(util=None), dict(cu_ret=None), dict(k_out=None), dict(v_out=None),
+               dict(out_rows=-1), dict(budget=0), dict(prm=B.Params(pool_kernel=4).c())):
+        assert _compress(lib, pb, **kw) == B.EINVAL, kw
+    assert _compress(lib, pb, ws=None) == B.EWORKSPACE
+    assert _compress(lib, pb, ws_bytes=need - 256) == B.EWORKSPACE
+    assert _compress(lib, pb, ws=FAKE * 16 + 4) == B.EWORKSPACE
+    assert _compress(lib, _problem(d=96)) == B.EUNSUPPORTED
+    assert _compress(lib, _problem(W=65)) == B.EUNSUPPORTED
+
+
+def test_status_read_rejects(lib):
+    pb = _problem()  # no status word
+    flags = ctypes.c_uint32(0)
+    assert lib.stepkv_status_read(ctypes.byref(pb), ctypes.byref(flags), 0, None) == B.EINVAL
+    pb.status = FAKE
+    assert lib.stepkv_status_read(ctypes.byref(pb), None, 0, None) == B.EINVAL
+    assert lib.stepkv_status_read(None, ctypes.byref(flags), 0, None) == B.EINVAL

@@ -46,9 +46,15 @@ def test_compression_pass_replays_in_a_hip_graph(shared, gpu_lib):
             B.select(pb, scores, g.prot, g.sid, g.budget, idx=idx, cu_retained=cu_ret)
             B.compact(pb, g.k, g.v, idx, cu_ret, g.out_rows, k_out=k_out, v_out=v_out)
 
+    rows_s = np.diff(pb.retained_rows(w.protected, g.budget))
+
+    def defined(t):  # the entries select writes: the first R_s positions of each sequence
+        return torch.cat([t[..., int(w.cu_seqlens[s]):int(w.cu_seqlens[s]) + int(rows_s[s])]
+                          for s in range(w.num_seqs)], dim=-1)
+
     def snapshot():
         torch.cuda.synchronize()
-        return [t.clone() for t in (scores, idx, cu_ret, k_out, v_out)]
+        return [t.clone() for t in (scores, defined(idx), cu_ret, k_out, v_out)]
 
     log(f"[graph {'shared' if shared else 'per-head'}] rows={rows} eager reference")
     run()

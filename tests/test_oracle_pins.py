@@ -403,6 +403,21 @@ def test_select_all_equal_and_budget_edges():
     assert list(O.select_retained(P, ~np.zeros(7, bool), 0)) == []
 
 
+@pytest.mark.parametrize("seed", range(4))
+def test_retained_count_is_the_selection_size(seed):
+    """eq. problem with exactly min(B, N_pr) kept: the count equals the size of the
+    selection itself (which is pinned against Python's sorted()), protected tokens anywhere."""
+    rng = np.random.default_rng(40 + seed)
+    for _ in range(20):
+        n = int(rng.integers(0, 120))
+        prun = rng.random(n) > 0.3
+        B = int(rng.integers(1, 150))
+        P = rng.random(n)
+        assert O.retained_count(n, int((~prun).sum()), B) == len(O.select_retained(P, prun, B))
+    assert O.retained_count(10, 10, 5) == 10 and O.retained_count(0, 0, 3) == 0
+    assert O.retained_count(1000, 512, 1024) == 1000 and O.retained_count(4096, 512, 2048) == 2560
+
+
 def test_kept_per_step_sums_to_kept():
     rng = np.random.default_rng(3)
     sid = np.concatenate([np.full(5, -1), np.repeat(np.arange(6), 9)])
