@@ -76,6 +76,7 @@ extern "C" {
 #define STEPKV_EUNSUPPORTED (-2) /* valid but outside this build's limits */
 #define STEPKV_EWORKSPACE (-3)   /* workspace missing or too small */
 #define STEPKV_EHIP (-4)         /* a HIP launch or runtime call failed */
+#define STEPKV_ESCRATCH (-5)     /* the problem needs more than the static scratch */
 
 /* Limits of this build (STEPKV_EUNSUPPORTED beyond them). */
 #define STEPKV_MAX_WINDOW_ROWS 256   /* W * G */
@@ -322,6 +323,27 @@ int stepkv_score(const stepkv_problem* pb, const stepkv_params* prm, const void*
                  const void* k, const int32_t* step_ids, const uint8_t* protected_mask,
                  const float* step_utility, float* scores, float* saliency,
                  stepkv_step_stat* step_stats, void* workspace, size_t ws_bytes, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): stepkv_score
+ * with its workspace taken from a static device buffer of
+ * STEPKV_STATIC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends. The call allocates nothing and calls no allocating
+ * routine; the caller still passes every input and output, and `saliency`
+ * (fp32 [L][Hkv][Ntot], the A buffer the sweeps write) is required here.
+ * Same arguments, results and errors as stepkv_score otherwise, plus
+ * STEPKV_ESCRATCH when the problem needs more than the buffer
+ * (stepkv_saliency_workspace_bytes(pb) > STEPKV_STATIC_SCRATCH_BYTES), found
+ * before anything is launched. The first call on a device looks the buffer's
+ * address up (EHIP if that fails). Every call on one GPU shares its buffer,
+ * which keeps the last call's contents (no part of it needs to start at
+ * zero): calls that overlap on one GPU, on different streams or threads,
+ * race and must be ordered by the caller. */
+#define STEPKV_STATIC_SCRATCH_BYTES ((size_t)32 << 20)
+int stepkv_score_noalloc(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                         const void* k, const int32_t* step_ids, const uint8_t* protected_mask,
+                         const float* step_utility, float* scores, float* saliency,
+                         stepkv_step_stat* step_stats, void* stream);
 
 /* stepkv_score with the saliency taken from given row log-sum-exps
  * (stepkv_saliency_from_lse, one sweep over K) instead of both sweeps.

@@ -15,7 +15,8 @@ import numpy as np
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstepkv.so")
 
-OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP, ESCRATCH = 0, -1, -2, -3, -4, -5
+STATIC_SCRATCH_BYTES = 32 << 20  # STEPKV_STATIC_SCRATCH_BYTES
 FLAG_STEP_ID, FLAG_NONFINITE, FLAG_OUT_ROWS = 1, 2, 4  # STEPKV_FLAG_*
 CUE_CAP = 64  # STEPKV_CUE_CAP
 MAX_WINDOW_ROWS = 256
@@ -98,6 +99,8 @@ _SIGNATURES = {
     "stepkv_status_read": (ctypes.c_int, [ctypes.POINTER(ProblemC),
                                           ctypes.POINTER(ctypes.c_uint32), ctypes.c_int32, _vp]),
     "stepkv_compress_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
+    "stepkv_score_noalloc": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC),
+                                            _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "stepkv_compress": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp, _vp,
                                        _vp, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp,
                                        _vp, ctypes.c_int32, _vp, _vp, _vp, ctypes.c_size_t, _vp]),

@@ -152,6 +152,7 @@ const char* stepkv_strerror(int code) {
     case STEPKV_EUNSUPPORTED: return "unsupported shape or parameter";
     case STEPKV_EWORKSPACE: return "workspace missing or too small";
     case STEPKV_EHIP: return "HIP launch or runtime error";
+    case STEPKV_ESCRATCH: return "problem needs more than the static scratch";
     default: return "unknown error";
   }
 }
@@ -429,6 +430,29 @@ int stepkv_score(const stepkv_problem* pb, const stepkv_params* prm, const void*
   if (rc != STEPKV_OK) return rc;
   return run_priority(pb, prm, sal, step_ids, protected_mask, step_utility, scores, step_stats,
                       st);
+}
+
+int stepkv_score_noalloc(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
+                         const void* k, const int32_t* step_ids, const uint8_t* protected_mask,
+                         const float* step_utility, float* scores, float* saliency,
+                         stepkv_step_stat* step_stats, void* stream) {
+  static_assert(STEPKV_STATIC_SCRATCH_BYTES == kStaticScratchBytes, "one scratch size");
+  int rc = check_problem(pb);
+  if (rc == STEPKV_OK) rc = check_params(pb, prm);
+  if (rc != STEPKV_OK) return rc;
+  if (!q_win || !k || !saliency) return STEPKV_EINVAL;
+  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats);
+  if (rc != STEPKV_OK) return rc;
+  // the sweeps' workspace (everything but the saliency buffer, which the caller passes)
+  if (layout(pb, plan_saliency(pb)).sal > kStaticScratchBytes) return STEPKV_ESCRATCH;
+  if (pb->cu_seqlens_host[pb->num_seqs] == 0) return STEPKV_OK;
+  void* ws = nullptr;
+  if (static_scratch(&ws) != hipSuccess || !ws) return STEPKV_EHIP;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  rc = run_saliency(pb, prm, q_win, k, saliency, static_cast<uint8_t*>(ws), st);
+  if (rc != STEPKV_OK) return rc;
+  return run_priority(pb, prm, saliency, step_ids, protected_mask, step_utility, scores,
+                      step_stats, st);
 }
 
 int stepkv_window_lse(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,

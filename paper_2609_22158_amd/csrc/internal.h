@@ -105,6 +105,11 @@ hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
 // a captured graph).
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int n, hipStream_t st);
 
+// The static device scratch of stepkv_score_noalloc (STEPKV_STATIC_SCRATCH_BYTES):
+// its address on the current device, looked up on the first call per device.
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+hipError_t static_scratch(void** ptr);
+
 // Device status bits (the STEPKV_FLAG_* values of stepkv.h).
 constexpr uint32_t kFlagStepId = 1u, kFlagNonFinite = 2u, kFlagOutRows = 4u;
 

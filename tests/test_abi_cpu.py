@@ -31,7 +31,7 @@ def _declared_functions():
 
 def test_exports_every_declared_function(lib):
     names = _declared_functions()
-    assert len(names) == 28, names
+    assert len(names) == 29, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGNATURES)
@@ -326,3 +326,31 @@ def test_status_read_rejects(lib):
     pb.status = FAKE
     assert lib.stepkv_status_read(ctypes.byref(pb), None, 0, None) == B.EINVAL
     assert lib.stepkv_status_read(None, ctypes.byref(flags), 0, None) == B.EINVAL
+
+
+def test_score_noalloc_rejects(lib):
+    """The scratch-only scoring validates like stepkv_score, needs the saliency buffer, and
+    refuses a problem whose sweep workspace exceeds the static scratch before launching."""
+    prm = B.Params().c()
+
+    def call(pb, p=prm, **kw):
+        a = dict(q=FAKE, k=FAKE, sid=FAKE, prot=FAKE, util=FAKE, scores=FAKE, sal=FAKE,
+                 stats=None)
+        a.update(kw)
+        return lib.stepkv_score_noalloc(ctypes.byref(pb), ctypes.byref(p) if p else None,
+                                        a["q"], a["k"], a["sid"], a["prot"], a["util"],
+                                        a["scores"], a["sal"], a["stats"], None)
+
+    pb = _problem()
+    assert call(pb, sal=None) == B.EINVAL  # the saliency buffer is required here
+    assert call(pb, p=None) == B.EINVAL
+    assert call(pb, q=None) == B.EINVAL
+    assert call(pb, scores=None) == B.EINVAL
+    assert call(_problem(d=96)) == B.EUNSUPPORTED
+    # 64 layers x 8 heads x 256 window rows over 64 sequences of 20000 tokens: the per-chunk
+    # partials alone exceed 32 MiB
+    big = _problem(L=64, Hq=32, Hkv=8, W=64, cu=tuple(range(0, 64 * 20000 + 1, 20000)),
+                   cu_steps=tuple(range(65)))
+    assert lib.stepkv_saliency_workspace_bytes(ctypes.byref(big)) > B.STATIC_SCRATCH_BYTES
+    assert call(big) == B.ESCRATCH
+    assert "static scratch" in B.strerror(B.ESCRATCH)
