@@ -291,7 +291,8 @@ def main():
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
-    pb = B.Problem.from_workload(w, dev)
+    # no device status word: its checks are a diagnostic, not part of the timed pass
+    pb = B.Problem.from_workload(w, dev, status=False)
     q, k, v = (B.bf16_from_bits(x, dev) for x in (w.q_win, w.k, w.v))
     sid = torch.from_numpy(w.step_ids).to(dev)
     prot = torch.from_numpy(w.protected).to(dev)

@@ -382,9 +382,9 @@ class Problem:
         return retained_rows(self, protected, budget, budgets)
 
     @classmethod
-    def from_workload(cls, w, device="cuda") -> "Problem":
+    def from_workload(cls, w, device="cuda", status: bool = True) -> "Problem":
         return cls(w.num_layers, w.num_q_heads, w.num_kv_heads, w.head_dim, w.window,
-                   w.cu_seqlens, w.cu_steps, device)
+                   w.cu_seqlens, w.cu_steps, device, status)
 
     @property
     def ntot(self) -> int:

@@ -55,6 +55,17 @@ __device__ __forceinline__ void report_flags(uint32_t* status, uint32_t bits) {
 // x is neither NaN nor infinite.
 __device__ __forceinline__ bool finite(float x) { return fabsf(x) <= 3.40282347e38f; }
 
+// ORs the STEPKV_FLAG_* bits of wave-wide condition masks (ballots kept in
+// scalar registers while the wave works) into the device status word: one
+// atomic per wave, none when no lane met a condition. Wave-uniform call.
+__device__ __forceinline__ void report_masks(uint32_t* status, uint64_t step_id_mask,
+                                             uint64_t nonfinite_mask) {
+  const uint32_t w = (step_id_mask ? 1u : 0u) | (nonfinite_mask ? 2u : 0u);
+  if (status != nullptr && w != 0u &&
+      (threadIdx.x & (kWave - 1)) == __builtin_ctzll(__ballot(1)))
+    atomicOr(status, w);
+}
+
 // 2^x on the transcendental unit (v_exp_f32); -inf gives 0.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 

@@ -36,10 +36,14 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   // contiguous range of heads. The grid is padded to a multiple of 8.
   const int per = (int)(gridDim.x >> 3);
   const int bid = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
-  if (bid >= a.LH * nb) return;
+  if (bid >= a.LH * nb) {
+    // the first block past the gather (the grid always has one) reports rows
+    // dropped past out_rows; the gather blocks carry no extra work for it
+    if (bid == a.LH * nb && threadIdx.x == 0 && a.status && a.cu_retained[a.S] > a.out_rows)
+      atomicOr(a.status, kFlagOutRows);
+    return;
+  }
   const int lh = bid / nb, rb = bid - lh * nb;
-  if (bid == 0 && threadIdx.x == 0 && a.status && a.cu_retained[a.S] > a.out_rows)
-    atomicOr(a.status, kFlagOutRows);  // the rows past out_rows are dropped
   const int total = min(a.out_rows, a.cu_retained[a.S]);
   const int sub = threadIdx.x / kLanesPerRow, piece = threadIdx.x % kLanesPerRow;
   const size_t in_head = (size_t)lh * a.ntot;
@@ -114,9 +118,9 @@ hipError_t launch_compact(const CompactArgs& a, hipStream_t st) {
                          a.out_rows, a.status);
     return hipGetLastError();
   }
-  auto grid = [&](int rows_per_block) {  // a multiple of 8: one eighth per XCD
+  auto grid = [&](int rows_per_block) {  // a multiple of 8 (one eighth per XCD), one spare block
     const unsigned nb = (unsigned)((a.out_rows + rows_per_block - 1) / rows_per_block);
-    return dim3(((unsigned)a.LH * nb + 7u) / 8u * 8u);
+    return dim3(((unsigned)a.LH * nb + 1u + 7u) / 8u * 8u);
   };
   if (a.d == 128)
     hipLaunchKernelGGL(compact_kernel<128>, grid(rows_per_block<128>()), dim3(kThreads), 0, st, a);

@@ -2,14 +2,11 @@
 // q . K_hat^T) V_hat for every (layer, sequence, query head), fp32
 // accumulation (the consumer of the compacted cache, Sec. 3).
 //
-// decode_split_kernel: one workgroup per (layer, KV head, sequence, split of
-// 512 retained rows) serves all G query heads of the KV head, so K and V are
-// read once. 16-byte pieces, 2d/16 lanes per row (coalesced rows), the next
-// four rows' loads issued before the current four rows' arithmetic; q . k from
-// the raw bf16 pairs (v_dot2 with fp32 sums, scale applied after), an exact
-// online softmax per head in the log2 domain; a row's lanes sum by DPP, lane
-// groups merge by shuffles, waves in LDS, and decode_combine_kernel merges the
-// splits. decode_simple_kernel serves groups wider than 8 query heads.
+// decode_mfma_kernel: one workgroup per (layer, KV head, sequence, split of
+// 512 retained rows) serves all G <= 16 query heads of the KV head, so K and V
+// are read once: q . k for the whole query group on MFMA, an exact online
+// softmax per head, p V in fp32 on the vector units; decode_combine_kernel
+// merges the splits. decode_simple_kernel serves groups wider than 16 heads.
 #include "common.h"
 #include "internal.h"
 
@@ -101,47 +98,12 @@ constexpr int kSplitRows = STEPKV_DECODE_SPLIT_ROWS;  // retained rows per workg
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ bf16x2_t as_bf16x2(unsigned int w) {
-  return __builtin_bit_cast(bf16x2_t, w);
-}
-
 __device__ __forceinline__ void unpack8(const u32x4_t& w, float (&f)[8]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     f[2 * i] = __uint_as_float(w[i] << 16);
     f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
   }
-}
-
-// Sum over the LPR lanes of a row (8 or 16 consecutive lanes, one DPP row or
-// half-row) with DPP lane permutes: swap neighbours, swap pairs, mirror the
-// half-row, mirror the row. Every lane of the group ends with the sum.
-template <int LPR>
-__device__ __forceinline__ float row_sum(float v) {
-  static_assert(LPR == 8 || LPR == 16, "lanes per row");
-  auto dpp = [](float x, auto ctrl_c) __attribute__((always_inline)) {
-    constexpr int ctrl = decltype(ctrl_c)::value;
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), ctrl, 0xf, 0xf, false));
-  };
-  v += dpp(v, std::integral_constant<int, 0xb1>{});   // quad_perm [1,0,3,2]
-  v += dpp(v, std::integral_constant<int, 0x4e>{});   // quad_perm [2,3,0,1]
-  v += dpp(v, std::integral_constant<int, 0x141>{});  // row_half_mirror
-  if constexpr (LPR == 16) v += dpp(v, std::integral_constant<int, 0x140>{});  // row_mirror
-  return v;
-}
-
-// Merge online-softmax state (m, z, o) with another (log2 domain).
-template <int N>
-__device__ __forceinline__ void merge_state(float& m, float& z, float (&o)[N], float mo, float zo,
-                                            const float (&oo)[N]) {
-  const float mn = fmaxf(m, mo);
-  if (mn == -INFINITY) return;  // both empty
-  const float a = fast_exp2(m - mn), b = fast_exp2(mo - mn);
-  z = z * a + zo * b;
-#pragma unroll
-  for (int i = 0; i < N; ++i) o[i] = o[i] * a + oo[i] * b;
-  m = mn;
 }
 
 // Row splits of sequence s: ceil(min(N_s, out_rows) / kSplitRows).
@@ -179,15 +141,41 @@ __device__ __forceinline__ void locate_split(const DecodeArgs& a, int gs, int& s
   first_out = base;
 }
 
+typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef float f32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
+
+// One workgroup per (layer, KV head, sequence, split of kSplitRows retained
+// rows); each wave takes a quarter of the split in tiles of 16 rows and keeps
+// its own online-softmax state.
+//  - S = K_tile Q^T on v_mfma_f32_16x16x32_bf16: A = 16 key rows, B = the
+//    group's query heads (16 columns, heads past G are zero). The d axis is
+//    permuted so that lane l reads 2D/4 contiguous bytes of row l % 16 (the
+//    query uses the same permutation). Lane l then holds head l % 16 for rows
+//    4 (l / 16) + 0..3 of the tile.
+//  - Softmax per head in that layout: the tile maximum over the four lane
+//    groups, a reference per head that moves only when a logit passes it by
+//    more than 2^kSlack (so p <= 2^kSlack and rescaling is rare), p = 2^(x - m).
+//  - p goes through a per-wave LDS tile to the value lanes: 8 dims of one row
+//    per lane (coalesced 16-byte loads), o[g][:] += p[g][row] * v[row][:] in
+//    fp32 for the GM heads.
+// Waves merge in LDS; decode_combine_kernel merges the splits.
+constexpr float kSlack = 16.f;
+
 template <int D, int GM>
-__global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
-  constexpr int LPR = 2 * D / 16;        // lanes per 2d-byte row
-  constexpr int GPW = kWave / LPR;       // row groups per wave
-  constexpr int NG = (kThreads / kWave) * GPW;
-  constexpr int ST = D + 2;              // floats per head in a partial state: o[D], m, z
-  __shared__ float wstate[kThreads / kWave][GM][ST];
+__global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
+  constexpr int KS = D / 32;          // MFMA k-steps over d
+  constexpr int KQ = D / 4;           // d entries per lane group (q = lane / 16) and row
+  constexpr int LPR = D / 8;          // value lanes per row (8 dims each)
+  constexpr int RPL = kWave / LPR;    // value rows per load instruction
+  constexpr int VL = 16 / RPL;        // value loads per lane and tile
+  constexpr int NW = kThreads / kWave;
+  constexpr int ST = D + 2;           // floats per head in a partial state: o[D], m, z
+  static_assert(GM % 4 == 0 && GM <= 16, "heads per group");
+  __shared__ __attribute__((aligned(16))) float ptile[NW][16][16];  // p[row][head] per wave
+  __shared__ __attribute__((aligned(16))) float fscale[NW][16];     // rescale factors per head
+  __shared__ float wstate[NW][GM][ST];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int sub = lane % LPR, grp = wave * GPW + lane / LPR;
+  const int q = lane >> 4, c16 = lane & 15;
   const int lh = blockIdx.x / a.total_splits;
   const int gs = blockIdx.x - lh * a.total_splits;
   int s, first;
@@ -197,123 +185,138 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   const int l = lh / a.Hkv, h = lh - l * a.Hkv;
   const int r0 = a.cu_retained[s];
   const int R = max(0, min(a.cu_retained[s + 1], a.out_rows) - r0);
-  const int row_end = min(R, (j + 1) * kSplitRows);
-  // this lane's 8 dims (4 bf16 pairs) of every query head of the group
-  u32x4_t q[GM];
-  const float qs = a.scale * 1.44269504088896341f;  // logits in the log2 domain
+  constexpr int kWaveRows = kSplitRows / NW;
+  const int w0 = j * kSplitRows + wave * kWaveRows;  // this wave's rows [w0, w1)
+  const int w1 = min(R, w0 + kWaveRows);
+  // query heads as the B operand: head c16, d = q KQ + 8 ks + 0..7
+  bf16x8_t qb[KS];
 #pragma unroll
-  for (int g = 0; g < GM; ++g) {
-    q[g] = u32x4_t{0u, 0u, 0u, 0u};
-    if (g < a.G)
-      q[g] = *reinterpret_cast<const u32x4_t*>(
-          a.q + (((size_t)l * a.S + s) * a.Hq + h * a.G + g) * D + 8 * sub);
+  for (int ks = 0; ks < KS; ++ks) {
+    qb[ks] = bf16x8_t{};
+    if (c16 < a.G)
+      qb[ks] = *reinterpret_cast<const bf16x8_t*>(
+          a.q + (((size_t)l * a.S + s) * a.Hq + h * a.G + c16) * D + q * KQ + 8 * ks);
   }
-  float m[GM], z[GM], o[GM][8];
+  const float cl2 = a.scale * 1.44269504088896341f;  // logits in the log2 domain
+  float m_ref = -INFINITY;  // reference of head c16 (the same in the four lane groups)
+  float zp = 0.f;           // this lane's share of head c16's sum
+  float o[GM][8];
 #pragma unroll
-  for (int g = 0; g < GM; ++g) {
-    m[g] = -INFINITY;
-    z[g] = 0.f;
+  for (int g = 0; g < GM; ++g)
 #pragma unroll
     for (int i = 0; i < 8; ++i) o[g][i] = 0.f;
-  }
-  const u32x4_t* kb = reinterpret_cast<const u32x4_t*>(a.k + ((size_t)lh * a.out_rows + r0) * D);
-  const u32x4_t* vb = reinterpret_cast<const u32x4_t*>(a.v + ((size_t)lh * a.out_rows + r0) * D);
-  // one online-softmax update for NR rows r, r + NG, ...; rows at or past
-  // row_end re-read the first row and count as absent
-  constexpr int NR = 4;
-  auto update = [&](const u32x4_t (&kw)[NR], const u32x4_t (&vw)[NR], int r)
-      __attribute__((always_inline)) {
-    float v[NR][8];
+  const uint16_t* kb = a.k + ((size_t)lh * a.out_rows + r0) * D;
+  const uint16_t* vb = a.v + ((size_t)lh * a.out_rows + r0) * D;
+  const int vrow = lane / LPR, vcol = 8 * (lane % LPR);
+  // the tile at row t: K as the MFMA A operand, V as 8 dims of a row per lane;
+  // rows past the end re-read the last one
+  auto load = [&](int t, bf16x8_t (&ka)[KS], u32x4_t (&vw)[VL]) __attribute__((always_inline)) {
+    const int rk = min(t + c16, w1 - 1);
 #pragma unroll
-    for (int b = 0; b < NR; ++b) unpack8(vw[b], v[b]);
+    for (int ks = 0; ks < KS; ++ks)
+      ka[ks] = __builtin_nontemporal_load(
+          reinterpret_cast<const bf16x8_t*>(kb + (size_t)rk * D + q * KQ + 8 * ks));
 #pragma unroll
-    for (int g = 0; g < GM; ++g) {
-      if (g >= a.G) break;
-      float dt[NR];
-#pragma unroll
-      for (int b = 0; b < NR; ++b) {
-        float acc = 0.f;  // exact bf16 products, fp32 sums
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q[g][i]), as_bf16x2(kw[b][i]), acc,
-                                                false);
-        dt[b] = r + b * NG < row_end ? row_sum<LPR>(acc) * qs : -INFINITY;
-      }
-      float mn = m[g];
-#pragma unroll
-      for (int b = 0; b < NR; ++b) mn = fmaxf(mn, dt[b]);
-      const float sc = fast_exp2(m[g] - mn);
-      float p[NR], zs = 0.f;
-#pragma unroll
-      for (int b = 0; b < NR; ++b) {
-        p[b] = fast_exp2(dt[b] - mn);
-        zs += p[b];
-      }
-      z[g] = fmaf(z[g], sc, zs);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        float t = p[0] * v[0][i];
-#pragma unroll
-        for (int b = 1; b < NR; ++b) t = fmaf(p[b], v[b][i], t);
-        o[g][i] = fmaf(o[g][i], sc, t);
-      }
-      m[g] = mn;
+    for (int i = 0; i < VL; ++i) {
+      const int rv = min(t + i * RPL + vrow, w1 - 1);
+      vw[i] = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4_t*>(vb + (size_t)rv * D + vcol));
     }
   };
-  auto load = [&](int rr, u32x4_t (&kw)[NR], u32x4_t (&vw)[NR]) __attribute__((always_inline)) {
+  for (int t = w0; t < w1; t += 16) {  // wave-uniform loop
+    bf16x8_t ka[KS];
+    u32x4_t vw[VL];
+    load(t, ka, vw);
+    f32x4_t acc = f32x4_t{};
 #pragma unroll
-    for (int b = 0; b < NR; ++b) {
-      const int ri = rr + b * NG < row_end ? rr + b * NG : rr;
-      kw[b] = __builtin_nontemporal_load(kb + (size_t)ri * LPR + sub);
-      vw[b] = __builtin_nontemporal_load(vb + (size_t)ri * LPR + sub);
-    }
-  };
-  int r = j * kSplitRows + grp;
-  u32x4_t ck[NR], cv[NR];
-  if (r < row_end) load(r, ck, cv);
-  while (r < row_end) {  // the next rows' loads go out before this batch's arithmetic
-    const int rn = r + NR * NG;
-    u32x4_t nk[NR], nv[NR];
-    if (rn < row_end) load(rn, nk, nv);
-    update(ck, cv, r);
+    for (int ks = 0; ks < KS; ++ks)
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[ks], qb[ks], acc, 0, 0, 0);
+    float x[4];
 #pragma unroll
-    for (int b = 0; b < NR; ++b) {
-      ck[b] = nk[b];
-      cv[b] = nv[b];
+    for (int i = 0; i < 4; ++i) x[i] = t + 4 * q + i < w1 ? acc[i] * cl2 : -INFINITY;
+    float tmax = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    // -inf never moves the reference; the first finite tile does
+    if (__builtin_amdgcn_ballot_w64(tmax > m_ref + kSlack) != 0) {  // wave-uniform, rare
+      // the tile maximum of each head over its four lane groups
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
+      const bool move = tmax > m_ref + kSlack;  // the same in the four lane groups of a head
+      const float m_new = move ? tmax : m_ref;
+      const float f = m_ref == -INFINITY ? 0.f : fast_exp2(m_ref - m_new);
+      zp *= f;
+      m_ref = m_new;
+      if (q == 0) fscale[wave][c16] = f;
+      __builtin_amdgcn_wave_barrier();
+      float fs[GM];
+#pragma unroll
+      for (int g = 0; g < GM; g += 4) {
+        const float4 v4 = *reinterpret_cast<const float4*>(&fscale[wave][g]);
+        fs[g] = v4.x;
+        fs[g + 1] = v4.y;
+        fs[g + 2] = v4.z;
+        fs[g + 3] = v4.w;
+      }
+#pragma unroll
+      for (int g = 0; g < GM; ++g)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[g][i] *= fs[g];
     }
-    r = rn;
+    float p[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      p[i] = x[i] == -INFINITY ? 0.f : fast_exp2(x[i] - m_ref);
+      zp += p[i];
+      ptile[wave][4 * q + i][c16] = p[i];
+    }
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int i = 0; i < VL; ++i) {
+      const int rr = i * RPL + vrow;  // row of the tile
+      float pr[GM];
+#pragma unroll
+      for (int g = 0; g < GM; g += 4) {
+        const float4 v4 = *reinterpret_cast<const float4*>(&ptile[wave][rr][g]);
+        pr[g] = v4.x;
+        pr[g + 1] = v4.y;
+        pr[g + 2] = v4.z;
+        pr[g + 3] = v4.w;
+      }
+      float v[8];
+      unpack8(vw[i], v);
+#pragma unroll
+      for (int g = 0; g < GM; ++g)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[g][e] = fmaf(pr[g], v[e], o[g][e]);
+    }
+    __builtin_amdgcn_wave_barrier();  // the tile's p reads precede the next tile's writes
   }
-  // merge the row groups of this wave (lanes with the same piece)
+  // this wave's sums: z over the four lane groups, o over the row groups of the value lanes
+  zp += __shfl_xor(zp, 16, kWave);
+  zp += __shfl_xor(zp, 32, kWave);
 #pragma unroll
-  for (int off = LPR; off < kWave; off <<= 1) {
+  for (int off = LPR; off < kWave; off <<= 1)
 #pragma unroll
-    for (int g = 0; g < GM; ++g) {
-      if (g >= a.G) break;
-      float oo[8];
+    for (int g = 0; g < GM; ++g)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) oo[i] = __shfl_xor(o[g][i], off, kWave);
-      const float mo = __shfl_xor(m[g], off, kWave), zo = __shfl_xor(z[g], off, kWave);
-      merge_state(m[g], z[g], o[g], mo, zo, oo);
-    }
-  }
+      for (int i = 0; i < 8; ++i) o[g][i] += __shfl_xor(o[g][i], off, kWave);
   if (lane < LPR) {
 #pragma unroll
     for (int g = 0; g < GM; ++g) {
       if (g >= a.G) break;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) wstate[wave][g][8 * sub + i] = o[g][i];
-      if (sub == 0) {
-        wstate[wave][g][D] = m[g];
-        wstate[wave][g][D + 1] = z[g];
-      }
+      for (int i = 0; i < 8; ++i) wstate[wave][g][vcol + i] = o[g][i];
     }
+  }
+  if (q == 0 && c16 < a.G) {
+    wstate[wave][c16][D] = m_ref;
+    wstate[wave][c16][D + 1] = zp;
   }
   __syncthreads();
   // merge the waves: thread (g, d) for every head g and dim d
   for (int e = tid; e < a.G * D; e += kThreads) {
     const int g = e / D, dd = e - g * D;
     float M = -INFINITY, Z = 0.f, O = 0.f;
-    for (int w = 0; w < kThreads / kWave; ++w) {
+    for (int w = 0; w < NW; ++w) {
       const float mw = wstate[w][g][D], zw = wstate[w][g][D + 1];
       const float mn = fmaxf(M, mw);
       if (mn == -INFINITY) continue;
@@ -342,8 +345,18 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(DecodeArgs a) {
   const int dd = threadIdx.x;
   if (blockIdx.x == 0 && dd == 0 && a.status && a.cu_retained[a.S] > a.out_rows)
     atomicOr(a.status, kFlagOutRows);  // the split kernel read no row past out_rows
-  int first = 0;  // global splits of the sequences before s (every lane adds them all)
-  for (int s2 = 0; s2 < s; ++s2) first += splits_of(a, s2);
+  // global splits of the sequences before s: a wave-wide prefix over 64 sequences at a time
+  int first = 0;
+  {
+    const int lane = dd & 63;
+    for (int s0 = 0; s0 < s; s0 += kWave) {
+      const int sq = s0 + lane;
+      int cnt = sq < s ? splits_of(a, sq) : 0;
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
+      first += cnt;
+    }
+  }
   const int last = first + splits_of(a, s);
   float M = -INFINITY, Z = 0.f, O = 0.f;
   for (int gs = first; gs < last; ++gs) {
@@ -371,12 +384,12 @@ int decode_total_splits(const int32_t* cu_seqlens_host, int S, int out_rows) {
 }
 
 size_t decode_partial_floats(const DecodeArgs& a) {
-  if (a.G > 8) return 0;
+  if (a.G > 16) return 0;
   return (size_t)a.L * a.Hkv * a.total_splits * a.G * (a.d + 2);
 }
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
-  if (a.G > 8) {  // wide query groups: one workgroup per query head
+  if (a.G > 16) {  // wide query groups: one workgroup per query head
     const dim3 grid((unsigned)(a.L * a.S * a.Hq));
     if (a.d == 128)
       hipLaunchKernelGGL(decode_simple_kernel<128>, grid, dim3(kThreads), 0, st, a);
@@ -386,12 +399,23 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
   }
   if (a.total_splits > 0) {
     const dim3 grid((unsigned)(a.L * a.Hkv) * (unsigned)a.total_splits);
+    auto go = [&](auto d_c, auto gm_c) {
+      constexpr int Dd = decltype(d_c)::value, GMm = decltype(gm_c)::value;
+      hipLaunchKernelGGL((decode_mfma_kernel<Dd, GMm>), grid, dim3(kThreads), 0, st, a);
+    };
+    using I128 = std::integral_constant<int, 128>;
+    using I64 = std::integral_constant<int, 64>;
+    using G4 = std::integral_constant<int, 4>;
+    using G8 = std::integral_constant<int, 8>;
+    using G16 = std::integral_constant<int, 16>;
     if (a.d == 128) {
-      if (a.G <= 4) hipLaunchKernelGGL((decode_split_kernel<128, 4>), grid, dim3(kThreads), 0, st, a);
-      else hipLaunchKernelGGL((decode_split_kernel<128, 8>), grid, dim3(kThreads), 0, st, a);
+      if (a.G <= 4) go(I128{}, G4{});
+      else if (a.G <= 8) go(I128{}, G8{});
+      else go(I128{}, G16{});
     } else {
-      if (a.G <= 4) hipLaunchKernelGGL((decode_split_kernel<64, 4>), grid, dim3(kThreads), 0, st, a);
-      else hipLaunchKernelGGL((decode_split_kernel<64, 8>), grid, dim3(kThreads), 0, st, a);
+      if (a.G <= 4) go(I64{}, G4{});
+      else if (a.G <= 8) go(I64{}, G8{});
+      else go(I64{}, G16{});
     }
   }
   const dim3 cgrid((unsigned)(a.L * a.S * a.Hq));

@@ -18,6 +18,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace stepkv {
 namespace {
 
@@ -72,7 +74,9 @@ __device__ __forceinline__ void write_stats(const FuseArgs& a, const StepTables&
   }
 }
 
-template <int HALF>
+// FLAGS: the conditions of STEPKV_FLAG_* are checked and reported (only when
+// the caller passed a status word; the unchecked instantiation carries none of it).
+template <int HALF, bool FLAGS>
 __global__ __launch_bounds__(kThreads) void fuse_batched_kernel(FuseArgs a) {
   // stage[kFastHalf + p] holds batch position p; runs of 8 positions are read
   // as aligned 16-byte vectors, global traffic stays coalesced (tid + 1024 j)
@@ -115,11 +119,9 @@ __global__ __launch_bounds__(kThreads) void fuse_batched_kernel(FuseArgs a) {
       pb[j] = prot[ic];
     }
   }
-  uint32_t bad = 0u;  // STEPKV_FLAG_* conditions met by this thread
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     const bool pr = ns > 0 && tid + kThreads * j < ns && pb[j] == 0;
-    bad |= pr && !finite(x[j]) ? kFlagNonFinite : 0u;
     x[j] = pr ? x[j] : 0.f;
     pb[j] = pr ? 1u : 0u;
   }
@@ -184,6 +186,9 @@ __global__ __launch_bounds__(kThreads) void fuse_batched_kernel(FuseArgs a) {
   // ---- sweep 2: normalise, fuse; the run's scores go back through the stage
   float* __restrict__ out = a.scores + (size_t)lh * a.ntot + seq0;
   int32_t* istage = reinterpret_cast<int32_t*>(stage);
+  // wave masks of the conditions met (STEPKV_FLAG_*): a prunable token with an
+  // out-of-range step id, or a non-finite priority (non-finite saliency or utility)
+  uint64_t bad_id = 0ull, bad_nf = 0ull;
 #pragma unroll
   for (int b = 0; b < kMaxBatches; ++b) {
     if (b < nb) {
@@ -204,8 +209,11 @@ __global__ __launch_bounds__(kThreads) void fuse_batched_kernel(FuseArgs a) {
         const bool ok = pr && kk >= 0 && kk < nsteps;
         const float th = u[b][r] * inv;
         const float util = ok ? tabs.util[ok ? kk : 0] : 0.f;
-        bad |= (pr && !ok ? kFlagStepId : 0u) | (!finite(util) ? kFlagNonFinite : 0u);
         pv[r] = pr ? fmaf(a.alpha, th, a.beta * util) : -INFINITY;
+        if (FLAGS) {
+          bad_id |= __ballot(pr && !ok);
+          bad_nf |= __ballot(pr && !finite(pv[r]));
+        }
         if (stats) {
           const int key = ok ? kk : -1;
           if (key != cur) {
@@ -236,7 +244,7 @@ __global__ __launch_bounds__(kThreads) void fuse_batched_kernel(FuseArgs a) {
       __syncthreads();  // the next batch reuses the stage
     }
   }
-  report_flags(a.status, bad);
+  if (FLAGS) report_masks(a.status, bad_id, bad_nf);
   if (stats) {
     __syncthreads();
     write_stats(a, tabs, lh, st0, nsteps);
@@ -512,13 +520,21 @@ hipError_t launch_fuse(const FuseArgs& a, hipStream_t st) {
   if (a.stats) dyn = ((size_t)(3 * a.max_steps) * 4 + 7) / 8 * 8 + (size_t)a.max_steps * 8;
   const dim3 grid(a.S * a.LH), block(kThreads);
   if (a.max_len <= kBatch * kMaxBatches && a.half <= kFastHalf) {
-    switch (a.half) {
-      case 0: hipLaunchKernelGGL(fuse_batched_kernel<0>, grid, block, dyn, st, a); break;
-      case 1: hipLaunchKernelGGL(fuse_batched_kernel<1>, grid, block, dyn, st, a); break;
-      case 2: hipLaunchKernelGGL(fuse_batched_kernel<2>, grid, block, dyn, st, a); break;
-      case 3: hipLaunchKernelGGL(fuse_batched_kernel<3>, grid, block, dyn, st, a); break;
-      default: hipLaunchKernelGGL(fuse_batched_kernel<4>, grid, block, dyn, st, a); break;
-    }
+    auto go = [&](auto half_c, auto flags_c) {
+      hipLaunchKernelGGL((fuse_batched_kernel<decltype(half_c)::value, decltype(flags_c)::value>),
+                         grid, block, dyn, st, a);
+    };
+    auto with_half = [&](auto flags_c) {
+      switch (a.half) {
+        case 0: go(std::integral_constant<int, 0>{}, flags_c); break;
+        case 1: go(std::integral_constant<int, 1>{}, flags_c); break;
+        case 2: go(std::integral_constant<int, 2>{}, flags_c); break;
+        case 3: go(std::integral_constant<int, 3>{}, flags_c); break;
+        default: go(std::integral_constant<int, 4>{}, flags_c); break;
+      }
+    };
+    if (a.status) with_half(std::true_type{});
+    else with_half(std::false_type{});
   } else {
     hipLaunchKernelGGL(fuse_stream_kernel, grid, block, dyn, st, a);
   }

@@ -3,8 +3,9 @@ attention (the oracle's decode_attention), within 2e-3 of each row's largest mag
 
 The caches here are seeded random rows laid out as the compaction writes them, with
 ragged retained counts (0, 1, and several 256-row splits) and query groups of 1, 4, 7
-and 16 heads per KV head; the last exceeds the grouped kernel's 8 and takes the
-per-head kernel."""
+12, 16 and 32 heads per KV head (the last wider than the grouped kernel's 16, so the
+per-head kernel), and one case whose logits spread over ~100 nats, so the running
+reference of each head moves in the middle of a split."""
 import math
 import zlib
 
@@ -19,12 +20,17 @@ from tests.gpu_cases import log
 pytestmark = pytest.mark.gpu
 
 CASES = {
-    # name: (L, Hq, Hkv, d, retained rows per sequence, out_rows slack)
-    "g4_d128_splits": (2, 32, 8, 128, [1536, 700, 1, 0, 257], 0),
-    "g7_d128": (2, 28, 4, 128, [2560, 31, 513], 5),
-    "g1_d64": (3, 4, 4, 64, [300, 64, 0, 1000], 0),
-    "g16_d128_wide": (1, 32, 2, 128, [900, 3], 0),
-    "g2_d64": (1, 4, 2, 64, [256, 255, 257], 0),
+    # name: (L, Hq, Hkv, d, retained rows per sequence, out_rows slack, key scale)
+    "g4_d128_splits": (2, 32, 8, 128, [1536, 700, 1, 0, 257], 0, 3.0),
+    "g7_d128": (2, 28, 4, 128, [2560, 31, 513], 5, 3.0),
+    "g1_d64": (3, 4, 4, 64, [300, 64, 0, 1000], 0, 3.0),
+    "g16_d128": (1, 32, 2, 128, [900, 3], 0, 3.0),
+    "g2_d64": (1, 4, 2, 64, [256, 255, 257], 0, 3.0),
+    "g8_d64": (2, 16, 2, 64, [1100, 17, 16, 15], 0, 3.0),
+    "g12_d128": (1, 24, 2, 128, [530, 47], 0, 3.0),  # 12 of the 16 MFMA columns in use
+    "g32_d128_wide": (1, 32, 1, 128, [700, 2], 0, 3.0),  # wider than 16: the per-head kernel
+    # logits spread over ~100 nats, so the per-head reference moves within a split
+    "g7_d128_peaky": (1, 14, 2, 128, [1400, 600], 0, 40.0),
 }
 
 
@@ -32,7 +38,7 @@ CASES = {
 def test_decode_matches_textbook_attention(cid):
     import torch
 
-    L, Hq, Hkv, d, rows, slack = CASES[cid]
+    L, Hq, Hkv, d, rows, slack, kscale = CASES[cid]
     G = Hq // Hkv
     S = len(rows)
     rng = np.random.default_rng(zlib.crc32(cid.encode()))
@@ -42,7 +48,7 @@ def test_decode_matches_textbook_attention(cid):
     cu_seq = np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32)
     pb = B.Problem(L, Hq, Hkv, d, 1, cu_seq, np.zeros(S + 1, np.int32))
     qb = f32_to_bf16_bits(rng.standard_normal((L, S, Hq, d)).astype(np.float32))
-    kb = f32_to_bf16_bits((rng.standard_normal((L, Hkv, out_rows, d)) / math.sqrt(d) * 3).astype(np.float32))
+    kb = f32_to_bf16_bits((rng.standard_normal((L, Hkv, out_rows, d)) / math.sqrt(d) * kscale).astype(np.float32))
     vb = f32_to_bf16_bits(rng.standard_normal((L, Hkv, out_rows, d)).astype(np.float32))
     log(f"[decode {cid}] L={L} Hq={Hq} Hkv={Hkv} d={d} rows={rows}")
     out = B.decode_attention(pb, B.bf16_from_bits(qb), B.bf16_from_bits(kb), B.bf16_from_bits(vb),
