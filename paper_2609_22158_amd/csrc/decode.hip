@@ -161,6 +161,19 @@ typedef float f32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
 // Waves merge in LDS; decode_combine_kernel merges the splits.
 constexpr float kSlack = 16.f;
 
+// Cross-lane exchanges on the vector unit (no LDS round trip): the value of
+// lane l ^ 16 and of lane l ^ 32 (gfx950 permlane swaps).
+__device__ __forceinline__ float xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  // lanes of even rows get the odd row's value in r[1], lanes of odd rows in r[0]
+  return __uint_as_float(((threadIdx.x >> 4) & 1) ? r[0] : r[1]);
+}
+__device__ __forceinline__ float xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(((threadIdx.x >> 5) & 1) ? r[0] : r[1]);
+}
 template <int D, int GM>
 __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
   constexpr int KS = D / 32;          // MFMA k-steps over d
@@ -227,6 +240,9 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
     bf16x8_t ka[KS];
     u32x4_t vw[VL];
     load(t, ka, vw);
+    // every load of the tile is in flight before the first wait (one memory
+    // round trip per tile, not one for K and another for V)
+    __builtin_amdgcn_sched_barrier(0);
     f32x4_t acc = f32x4_t{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
@@ -238,8 +254,8 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
     // -inf never moves the reference; the first finite tile does
     if (__builtin_amdgcn_ballot_w64(tmax > m_ref + kSlack) != 0) {  // wave-uniform, rare
       // the tile maximum of each head over its four lane groups
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
+      tmax = fmaxf(tmax, xor16(tmax));
+      tmax = fmaxf(tmax, xor32(tmax));
       const bool move = tmax > m_ref + kSlack;  // the same in the four lane groups of a head
       const float m_new = move ? tmax : m_ref;
       const float f = m_ref == -INFINITY ? 0.f : fast_exp2(m_ref - m_new);
@@ -291,8 +307,8 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
     __builtin_amdgcn_wave_barrier();  // the tile's p reads precede the next tile's writes
   }
   // this wave's sums: z over the four lane groups, o over the row groups of the value lanes
-  zp += __shfl_xor(zp, 16, kWave);
-  zp += __shfl_xor(zp, 32, kWave);
+  zp += xor16(zp);
+  zp += xor32(zp);
 #pragma unroll
   for (int off = LPR; off < kWave; off <<= 1)
 #pragma unroll
@@ -359,15 +375,29 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(DecodeArgs a) {
   }
   const int last = first + splits_of(a, s);
   float M = -INFINITY, Z = 0.f, O = 0.f;
-  for (int gs = first; gs < last; ++gs) {
-    const float* part = a.partial + (((size_t)lh * a.total_splits + gs) * a.G + g) * ST;
-    const float mw = part[D], zw = part[D + 1];
-    const float mn = fmaxf(M, mw);
-    if (mn == -INFINITY) continue;
-    const float x = fast_exp2(M - mn), y = fast_exp2(mw - mn);
-    Z = Z * x + zw * y;
-    O = O * x + part[dd] * y;
-    M = mn;
+  for (int g0 = first; g0 < last; g0 += 8) {  // eight splits' loads in flight at a time
+    float mw[8], zw[8], ow[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      mw[u] = -INFINITY;
+      zw[u] = 0.f;
+      ow[u] = 0.f;
+      if (g0 + u < last) {
+        const float* part = a.partial + (((size_t)lh * a.total_splits + g0 + u) * a.G + g) * ST;
+        mw[u] = part[D];
+        zw[u] = part[D + 1];
+        ow[u] = part[dd];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float mn = fmaxf(M, mw[u]);
+      if (mn == -INFINITY) continue;
+      const float x = fast_exp2(M - mn), y = fast_exp2(mw[u] - mn);
+      Z = Z * x + zw[u] * y;
+      O = O * x + ow[u] * y;
+      M = mn;
+    }
   }
   a.out[(((size_t)l * a.S + s) * a.Hq + hq) * D + dd] = Z > 0.f ? O / Z : 0.f;
 }
