@@ -11,7 +11,10 @@ line.
 
 The K timed steps carry no event inside a step. Per-stage times (HIP events
 around each C ABI call, on the launch stream) and the saliency roofline come
-from a second pass of the same K steps.
+from a second pass of the same K steps. A third pass writes --flush-mib bytes
+before each step (evicting the Infinity Cache) and times every step from the
+cold cache with its own events ("flushed"); "hbm_ceilings" gives the read and
+copy bandwidth of plain streaming kernels with the compaction's access width.
 
 By default the saliency is computed from the window queries and the cache
 alone (two sweeps over K). With --lse-fed the window rows' log-sum-exps are
@@ -69,6 +72,11 @@ def parse():
     ap.add_argument("--shared-layers", type=int, default=0,
                     help="shared-index mode: rank each sequence once from the saliency of its "
                          "last N layers and compact every layer and head with that one set")
+    ap.add_argument("--flush-mib", type=int, default=1024,
+                    help="bytes written before each step of the flushed timing pass (evicts the "
+                         "256 MB Infinity Cache); 0 skips that pass")
+    ap.add_argument("--ceiling-mib", type=int, default=1024,
+                    help="buffer size of the HBM read and copy ceiling probes; 0 skips them")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this size (HBM counter calibration)")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -223,6 +231,7 @@ def cpu_baseline(w, budget, seconds, params, lse_fed=False):
     per_head_rate = tokens / dt
     value = per_head_rate / (w.num_layers * w.num_kv_heads)
     return {"value": value, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "host_cpus": os.cpu_count(),
             "sample": f"{done} of {len(triples)} (sequence, layer, KV head) triples "
                       f"({tokens} token-heads) in {dt:.1f} s, scaled to all {w.num_layers} layers "
                       f"x {w.num_kv_heads} KV heads"}
@@ -253,6 +262,7 @@ def cpu_baseline_shared(w, budget, seconds, params, last_layers):
         if dt >= seconds:
             break
     return {"value": tokens / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "host_cpus": os.cpu_count(),
             "sample": f"{done} of {w.num_seqs} sequence(s) ({tokens} tokens), shared-index pass "
                       f"over the last {last_layers} layers and all {w.num_layers} layers' "
                       f"compaction, in {dt:.1f} s"}
@@ -298,9 +308,9 @@ def main():
     prot = torch.from_numpy(w.protected).to(dev)
     util = torch.empty(pb.total_steps, dtype=torch.float32, device=dev)
     # one pinned staging row per step of the run (warmup, timed pass, stage-timing
-    # pass), so that the host never overwrites a row whose copy may still be queued
-    # and no event has to be waited on inside a step
-    n_rows = args.warmup + 2 * args.steps
+    # pass, flushed pass), so that the host never overwrites a row whose copy may
+    # still be queued and no event has to be waited on inside a step
+    n_rows = args.warmup + 3 * args.steps
     util_pinned = torch.empty((n_rows, max(pb.total_steps, 1)), dtype=torch.float32,
                               pin_memory=True)
     slot = [0]
@@ -461,6 +471,49 @@ def main():
     stage_ms = {n: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
                 for i, n in enumerate(stage_names)}
 
+    # flushed pass: a write of --flush-mib before every step evicts the Infinity
+    # Cache, and per-step events time each step from a cold cache
+    flushed = None
+    if args.flush_mib > 0:
+        flush_buf = torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev)
+        fl_ms = []
+        for i in range(args.steps):
+            flush_buf.fill_(i & 0xFF)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            step()
+            e1.record(stream)
+            e1.synchronize()
+            fl_ms.append(e0.elapsed_time(e1))
+        del flush_buf
+        q10, q50, q90 = np.percentile(fl_ms, [10, 50, 90])
+        flushed = {"ms_per_step_median": round(float(q50), 4), "p10": round(float(q10), 4),
+                   "p90": round(float(q90), 4), "flush_bytes": args.flush_mib << 20,
+                   "value_median": round(float(ntot) / (q50 * 1e-3), 1)}
+    ceilings = None
+    if args.ceiling_mib > 0:  # plain streaming kernels with the compaction's access width
+        nb = args.ceiling_mib << 20
+        src_buf = torch.ones(nb, dtype=torch.uint8, device=dev)
+        dst_buf = torch.empty(nb, dtype=torch.uint8, device=dev)
+        res = {}
+        for name, copy in (("read", False), ("copy", True)):
+            for _ in range(3):
+                B.bandwidth_probe(src_buf, dst_buf, copy)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            reps = 20
+            e0.record(stream)
+            for _ in range(reps):
+                B.bandwidth_probe(src_buf, dst_buf, copy)
+            e1.record(stream)
+            e1.synchronize()
+            t = e0.elapsed_time(e1) * 1e-3 / reps
+            res[f"{name}_gbps"] = round(nb * (2 if copy else 1) / t / 1e9, 1)
+        res["bytes"] = nb
+        ceilings = res
+        del src_buf, dst_buf
+
     tokens = float(ntot)
     value = tokens / (ms_per_step * 1e-3)
     G = w.num_q_heads // Hkv
@@ -533,6 +586,10 @@ def main():
         "hbm": hbm,
         "roofline": roofline,
     }
+    if flushed:
+        line["flushed"] = flushed
+    if ceilings:
+        line["hbm_ceilings"] = ceilings
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = (cpu_baseline_shared(w, budget, args.cpu_seconds, params, n_sh)
                                 if shared else

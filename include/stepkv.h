@@ -470,6 +470,16 @@ int stepkv_decode_attention(const stepkv_problem* pb, const void* q_dec, const v
                             float scale, float* out, void* workspace, size_t ws_bytes,
                             void* stream);
 
+/* ---------------------------------------------------------------- measurement
+ * HBM ceiling probe (not part of the method): the bandwidth a plain streaming
+ * kernel reaches on this device with the access width of the compaction (one
+ * 16-byte non-temporal piece per thread), to set the measured kernels against.
+ * copy = 0: read `bytes` from src (dst receives at most bytes / 4096 words);
+ * copy != 0: copy `bytes` from src to dst (non-overlapping). bytes must be a
+ * positive multiple of 16 and the pointers 16-byte aligned. Asynchronous on
+ * `stream`. Errors: EINVAL, EHIP. */
+int stepkv_bandwidth_probe(const void* src, void* dst, size_t bytes, int32_t copy, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -104,6 +104,7 @@ _SIGNATURES = {
     "stepkv_compress": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp, _vp,
                                        _vp, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp,
                                        _vp, ctypes.c_int32, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "stepkv_bandwidth_probe": (ctypes.c_int, [_vp, _vp, ctypes.c_size_t, ctypes.c_int32, _vp]),
     "stepkv_score_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
     "stepkv_saliency_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
     "stepkv_saliency": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp,
@@ -798,6 +799,16 @@ def compress(pb: Problem, q_win, k, v, step_ids, protected, step_utility, budget
     _check("stepkv_compress", rc)
     return {"scores": scores, "idx": idx, "cu_retained": cu_retained, "k_hat": k_out,
             "v_hat": v_out}
+
+
+def bandwidth_probe(src, dst, copy: bool, stream=None) -> None:
+    """stepkv_bandwidth_probe: read src (copy False) or copy src to dst, with the
+    compaction's access width; both contiguous CUDA tensors, src.nbytes a multiple of 16."""
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < (nbytes if copy else 4 * ((nbytes // 16 + 255) // 256)):
+        raise ValueError("dst too small")
+    _check("stepkv_bandwidth_probe", load().stepkv_bandwidth_probe(
+        src.data_ptr(), dst.data_ptr(), nbytes, int(bool(copy)), _stream(stream)))
 
 
 def bf16_from_bits(bits: np.ndarray, device="cuda"):

@@ -700,6 +700,13 @@ int stepkv_compress(const stepkv_problem* pb, const stepkv_params* prm, const vo
   return stepkv_compact(pb, k, v, I, cu_retained, out_rows, k_out, v_out, stream);
 }
 
+int stepkv_bandwidth_probe(const void* src, void* dst, size_t bytes, int32_t copy, void* stream) {
+  if (!src || !dst || bytes == 0 || bytes % 16 != 0) return STEPKV_EINVAL;
+  if (reinterpret_cast<uintptr_t>(src) % 16 != 0 || reinterpret_cast<uintptr_t>(dst) % 16 != 0)
+    return STEPKV_EINVAL;
+  return hip_status(launch_probe(src, dst, bytes, copy, static_cast<hipStream_t>(stream)));
+}
+
 size_t stepkv_decode_workspace_bytes(const stepkv_problem* pb, int32_t out_rows) {
   if (check_problem(pb) != STEPKV_OK || out_rows < 0) return 0;
   DecodeArgs a{};

@@ -97,12 +97,47 @@ __global__ void out_rows_check_kernel(const int32_t* __restrict__ cu_retained, i
   if (threadIdx.x == 0 && cu_retained[S] > out_rows) atomicOr(status, kFlagOutRows);
 }
 
+// HBM ceiling probes: one 16-byte non-temporal piece per thread, the access
+// width and pattern of the compaction, over n16 pieces. Read: every piece is
+// loaded and folded into one word per block (so no load is dead). Copy: every
+// piece is loaded and stored.
+__global__ __launch_bounds__(kThreads) void probe_read_kernel(const u32x4_t* __restrict__ src,
+                                                              size_t n16, uint32_t* __restrict__ out) {
+  const size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
+  uint32_t x = 0u;
+  if (i < n16) {
+    const u32x4_t v = __builtin_nontemporal_load(src + i);
+    x = v[0] ^ v[1] ^ v[2] ^ v[3];
+  }
+  x = (uint32_t)wave_sum_int((int)x);
+  if ((threadIdx.x & (kWave - 1)) == 0 && x == 0x9e3779b9u) out[blockIdx.x] = x;  // rarely taken
+}
+
+__global__ __launch_bounds__(kThreads) void probe_copy_kernel(const u32x4_t* __restrict__ src,
+                                                              u32x4_t* __restrict__ dst, size_t n16) {
+  const size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i < n16) __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+}
+
 __global__ void fill_u32_kernel(uint32_t* __restrict__ p, uint32_t v, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = v;
 }
 
 }  // namespace
+
+hipError_t launch_probe(const void* src, void* dst, size_t bytes, int copy, hipStream_t st) {
+  const size_t n16 = bytes / 16;
+  if (n16 == 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((n16 + kThreads - 1) / kThreads);
+  if (copy)
+    hipLaunchKernelGGL(probe_copy_kernel, dim3(blocks), dim3(kThreads), 0, st,
+                       static_cast<const u32x4_t*>(src), static_cast<u32x4_t*>(dst), n16);
+  else
+    hipLaunchKernelGGL(probe_read_kernel, dim3(blocks), dim3(kThreads), 0, st,
+                       static_cast<const u32x4_t*>(src), n16, static_cast<uint32_t*>(dst));
+  return hipGetLastError();
+}
 
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int n, hipStream_t st) {
   if (n <= 0) return hipSuccess;

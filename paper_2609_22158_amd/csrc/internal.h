@@ -101,6 +101,11 @@ struct CompactArgs {
 };
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
 
+// HBM ceiling probe: read (copy = 0) or copy `bytes` (a multiple of 16) with
+// the compaction's access width; a read writes at most one word per block of
+// 256 threads to dst.
+hipError_t launch_probe(const void* src, void* dst, size_t bytes, int copy, hipStream_t st);
+
 // p[0 .. n) = v on the stream (a kernel, not a memset, so that it can sit in
 // a captured graph).
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int n, hipStream_t st);

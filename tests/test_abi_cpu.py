@@ -31,7 +31,7 @@ def _declared_functions():
 
 def test_exports_every_declared_function(lib):
     names = _declared_functions()
-    assert len(names) == 29, names
+    assert len(names) == 30, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGNATURES)
@@ -354,3 +354,12 @@ def test_score_noalloc_rejects(lib):
     assert lib.stepkv_saliency_workspace_bytes(ctypes.byref(big)) > B.STATIC_SCRATCH_BYTES
     assert call(big) == B.ESCRATCH
     assert "static scratch" in B.strerror(B.ESCRATCH)
+
+
+def test_bandwidth_probe_rejects(lib):
+    f = lib.stepkv_bandwidth_probe
+    assert f(None, FAKE, 1 << 20, 0, None) == B.EINVAL
+    assert f(FAKE, None, 1 << 20, 1, None) == B.EINVAL
+    assert f(FAKE, FAKE, 0, 0, None) == B.EINVAL
+    assert f(FAKE, FAKE, (1 << 20) + 8, 0, None) == B.EINVAL
+    assert f(FAKE + 8, FAKE, 1 << 20, 0, None) == B.EINVAL
