@@ -75,6 +75,49 @@ def build(verbose: bool = False, extra_flags=(), lib_path: str = LIB) -> str:
     return lib_path
 
 
+HOST_SOURCES = ["api.cpp", "step_text.cpp"]
+ASAN_LIB = os.path.join(BUILD + "_asan", "libstepkv_asan.so")
+
+
+def build_host_sanitized() -> str:
+    """libstepkv with its host C++ (argument validation, workspace planning, the step
+    utility and the text engine) built with AddressSanitizer and UndefinedBehaviorSanitizer
+    by g++, linked with the unsanitized HIP objects of the default build (device code is
+    not sanitized). Load it with the sanitizer runtime preloaded (see sanitizer_env)."""
+    if not all(os.path.exists(os.path.join(BUILD, src.rsplit(".", 1)[0] + ".o"))
+               for src in SOURCES):
+        build()
+    bdir = os.path.dirname(ASAN_LIB)
+    os.makedirs(bdir, exist_ok=True)
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(_hipcc())))
+    san = ["-fsanitize=address,undefined", "-fno-omit-frame-pointer", "-fno-sanitize-recover=all"]
+    objs = []
+    for src in HOST_SOURCES:
+        obj = os.path.join(bdir, src.rsplit(".", 1)[0] + ".o")
+        _run(["g++", "-std=c++17", "-O1", "-g", "-fPIC", "-Wall", "-D__HIP_PLATFORM_AMD__",
+              *san, f"-I{rocm}/include", f"-I{INCLUDE}", f"-I{CSRC}", "-c",
+              os.path.join(CSRC, src), "-o", obj])
+        objs.append(obj)
+    hip_objs = [os.path.join(BUILD, src.rsplit(".", 1)[0] + ".o") for src in SOURCES
+                if src not in HOST_SOURCES]
+    tmp = ASAN_LIB + ".tmp"
+    _run(["g++", "-shared", "-fPIC", *san, "-o", tmp, *objs, *hip_objs, f"-L{rocm}/lib",
+          "-lamdhip64", f"-Wl,-rpath,{rocm}/lib"])
+    os.replace(tmp, ASAN_LIB)
+    return ASAN_LIB
+
+
+def sanitizer_env() -> dict:
+    """Environment for a Python process that loads the sanitized library."""
+    asan = subprocess.run(["g++", "-print-file-name=libasan.so"], capture_output=True,
+                          text=True).stdout.strip()
+    env = dict(os.environ)
+    env.update({"LD_PRELOAD": asan, "STEPKV_LIB": ASAN_LIB, "PYTHONMALLOC": "malloc",
+                "ASAN_OPTIONS": "detect_leaks=0:halt_on_error=1:abort_on_error=0:exitcode=86",
+                "UBSAN_OPTIONS": "halt_on_error=1:print_stacktrace=1:exitcode=87"})
+    return env
+
+
 def build_c_demo() -> str:
     """Compile the plain-C consumer of the ABI (tests/c_abi) against the in-tree library."""
     rocm = os.path.dirname(os.path.dirname(os.path.realpath(_hipcc())))
