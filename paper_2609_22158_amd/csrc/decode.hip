@@ -198,6 +198,9 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
   const int l = lh / a.Hkv, h = lh - l * a.Hkv;
   const int r0 = a.cu_retained[s];
   const int R = max(0, min(a.cu_retained[s + 1], a.out_rows) - r0);
+  // splits are sized by the token count N_s, an upper bound of R known to the
+  // host; those past the retained rows hold no row and write no state
+  if (j * kSplitRows >= R) return;  // uniform over the workgroup
   constexpr int kWaveRows = kSplitRows / NW;
   const int w0 = j * kSplitRows + wave * kWaveRows;  // this wave's rows [w0, w1)
   const int w1 = min(R, w0 + kWaveRows);
@@ -373,7 +376,9 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(DecodeArgs a) {
       first += cnt;
     }
   }
-  const int last = first + splits_of(a, s);
+  // only the splits that hold retained rows wrote a state
+  const int R = max(0, min(a.cu_retained[s + 1], a.out_rows) - a.cu_retained[s]);
+  const int last = first + min(splits_of(a, s), (R + kSplitRows - 1) / kSplitRows);
   float M = -INFINITY, Z = 0.f, O = 0.f;
   for (int g0 = first; g0 < last; g0 += 8) {  // eight splits' loads in flight at a time
     float mw[8], zw[8], ow[8];
