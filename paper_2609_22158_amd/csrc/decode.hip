@@ -24,6 +24,13 @@ __device__ __forceinline__ float bf16_to_float(uint16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
+// Retained rows [r0, r0 + R) of sequence s, clamped to [0, out_rows) so that
+// no cu_retained value leads a read out of the cache.
+__device__ __forceinline__ int rows_of(const DecodeArgs& a, int s, int& r0) {
+  r0 = min(max(a.cu_retained[s], 0), a.out_rows);
+  return min(max(a.cu_retained[s + 1], r0), a.out_rows) - r0;
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void decode_simple_kernel(DecodeArgs a) {
   constexpr int kParts = kThreads / D;
@@ -38,9 +45,8 @@ __global__ __launch_bounds__(kThreads) void decode_simple_kernel(DecodeArgs a) {
   const int lh = l * a.Hkv + hq / a.G;
   if (blockIdx.x == 0 && tid == 0 && a.status && a.cu_retained[a.S] > a.out_rows)
     atomicOr(a.status, kFlagOutRows);  // rows past out_rows are not read
-  const int r0 = a.cu_retained[s];
-  const int r1 = min(a.cu_retained[s + 1], a.out_rows);
-  const int R = max(0, r1 - r0);
+  int r0;
+  const int R = rows_of(a, s, r0);
   const uint16_t* kb = a.k + ((size_t)lh * a.out_rows + r0) * D;
   const uint16_t* vb = a.v + ((size_t)lh * a.out_rows + r0) * D;
   const uint16_t* qp = a.q + (((size_t)l * a.S + s) * a.Hq + hq) * D;
@@ -106,14 +112,15 @@ __device__ __forceinline__ void unpack8(const u32x4_t& w, float (&f)[8]) {
   }
 }
 
-// Row splits of sequence s: ceil(min(N_s, out_rows) / kSplitRows).
+// Row splits of sequence s: ceil(R_s / kSplitRows).
 __device__ __forceinline__ int splits_of(const DecodeArgs& a, int s) {
-  const int n = min(a.cu_seqlens[s + 1] - a.cu_seqlens[s], a.out_rows);
-  return (n + kSplitRows - 1) / kSplitRows;
+  int r0;
+  return (rows_of(a, s, r0) + kSplitRows - 1) / kSplitRows;
 }
 
 // The sequence holding global split gs, and the first global split of that
-// sequence: a wave-wide prefix sum over 64 sequences at a time.
+// sequence: a wave-wide prefix sum over 64 sequences at a time. s_out = -1
+// when gs is past the last split (the grid is sized by a host-side bound).
 __device__ __forceinline__ void locate_split(const DecodeArgs& a, int gs, int& s_out,
                                              int& first_out) {
   const int lane = threadIdx.x & 63;
@@ -137,7 +144,7 @@ __device__ __forceinline__ void locate_split(const DecodeArgs& a, int gs, int& s
     }
     base += total;
   }
-  s_out = a.S - 1;  // not reached for gs < total_splits
+  s_out = -1;
   first_out = base;
 }
 
@@ -194,13 +201,11 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
   int s, first;
   locate_split(a, gs, s, first);
   s = uniform(s);
+  if (s < 0) return;  // past the last split: uniform over the workgroup
   const int j = uniform(gs - first);
   const int l = lh / a.Hkv, h = lh - l * a.Hkv;
-  const int r0 = a.cu_retained[s];
-  const int R = max(0, min(a.cu_retained[s + 1], a.out_rows) - r0);
-  // splits are sized by the token count N_s, an upper bound of R known to the
-  // host; those past the retained rows hold no row and write no state
-  if (j * kSplitRows >= R) return;  // uniform over the workgroup
+  int r0;
+  const int R = rows_of(a, s, r0);
   constexpr int kWaveRows = kSplitRows / NW;
   const int w0 = j * kSplitRows + wave * kWaveRows;  // this wave's rows [w0, w1)
   const int w1 = min(R, w0 + kWaveRows);
@@ -376,9 +381,8 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(DecodeArgs a) {
       first += cnt;
     }
   }
-  // only the splits that hold retained rows wrote a state
-  const int R = max(0, min(a.cu_retained[s + 1], a.out_rows) - a.cu_retained[s]);
-  const int last = first + min(splits_of(a, s), (R + kSplitRows - 1) / kSplitRows);
+  first = min(first, a.total_splits);  // the splits the grid held
+  const int last = min(first + splits_of(a, s), a.total_splits);
   float M = -INFINITY, Z = 0.f, O = 0.f;
   for (int g0 = first; g0 < last; g0 += 8) {  // eight splits' loads in flight at a time
     float mw[8], zw[8], ow[8];
@@ -409,13 +413,16 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(DecodeArgs a) {
 
 }  // namespace
 
+// A bound of sum_s ceil(R_s / kSplitRows) from what the host knows: R_s <=
+// min(N_s, out_rows), and sum_s R_s <= out_rows gives at most
+// floor(out_rows / kSplitRows) + S splits.
 int decode_total_splits(const int32_t* cu_seqlens_host, int S, int out_rows) {
-  int acc = 0;
+  int64_t acc = 0;
   for (int s = 0; s < S; ++s) {
     const int n = std::min(cu_seqlens_host[s + 1] - cu_seqlens_host[s], out_rows);
     acc += (n + kSplitRows - 1) / kSplitRows;
   }
-  return acc;
+  return (int)std::min<int64_t>(acc, (int64_t)(out_rows / kSplitRows) + S);
 }
 
 size_t decode_partial_floats(const DecodeArgs& a) {

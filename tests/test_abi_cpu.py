@@ -195,6 +195,18 @@ def test_select_compact_decode_reject(lib):
                                        float("inf"), FAKE, FAKE * 16, 1 << 20, None) == B.EINVAL
 
 
+def test_decode_workspace_counts_splits(lib):
+    """The decode workspace holds one fp32 state (o[d], m, z) per (layer, KV head, split, head
+    of the group); splits of 512 rows number min(sum_s ceil(min(N_s, out_rows) / 512),
+    floor(out_rows / 512) + S), the two bounds of sum_s ceil(R_s / 512) the host knows."""
+    per_split = 2 * 2 * 4 * (128 + 2) * 4  # L * Hkv * G * (d + 2) floats
+    for cu, out_rows, splits in [((0, 1000, 3000), 8, 2), ((0, 1000, 3000), 3000, 6),
+                                 ((0, 20000, 40000), 1026, 4), ((0, 20000, 40000), 1024, 4),
+                                 ((0, 20000, 40000), 1023, 3)]:
+        pb = _problem(cu=cu)
+        assert lib.stepkv_decode_workspace_bytes(ctypes.byref(pb), out_rows) == splits * per_split
+
+
 def test_lse_entry_points_reject(lib):
     """Validation of the LSE-fed calls: null arguments and short workspaces launch nothing."""
     pb = _problem()
