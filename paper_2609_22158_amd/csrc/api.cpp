@@ -714,7 +714,8 @@ size_t stepkv_decode_workspace_bytes(const stepkv_problem* pb, int32_t out_rows)
   a.Hkv = pb->num_kv_heads;
   a.G = pb->num_q_heads / pb->num_kv_heads;
   a.d = pb->head_dim;
-  a.total_splits = decode_total_splits(pb->cu_seqlens_host, pb->num_seqs, out_rows);
+  a.split_rows = decode_split_rows(a.L, a.Hkv, out_rows);
+  a.total_splits = decode_total_splits(pb->cu_seqlens_host, pb->num_seqs, out_rows, a.split_rows);
   return std::max<size_t>(sizeof(float) * decode_partial_floats(a), kAlign);
 }
 
@@ -745,7 +746,8 @@ int stepkv_decode_attention(const stepkv_problem* pb, const void* q_dec, const v
   a.G = pb->num_q_heads / pb->num_kv_heads;
   a.d = pb->head_dim;
   a.out_rows = out_rows;
-  a.total_splits = decode_total_splits(pb->cu_seqlens_host, pb->num_seqs, out_rows);
+  a.split_rows = decode_split_rows(a.L, a.Hkv, out_rows);
+  a.total_splits = decode_total_splits(pb->cu_seqlens_host, pb->num_seqs, out_rows, a.split_rows);
   a.scale = scale > 0.0f ? scale : (float)(1.0 / std::sqrt((double)pb->head_dim));
   return hip_status(launch_decode(a, static_cast<hipStream_t>(stream)));
 }

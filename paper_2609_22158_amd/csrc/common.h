@@ -66,6 +66,34 @@ __device__ __forceinline__ void report_masks(uint32_t* status, uint64_t step_id_
     atomicOr(status, w);
 }
 
+// Wait until at most N vector memory operations of this wave are outstanding
+// (they complete in issue order; direct-to-LDS loads count too).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Wait until at most `ahead` tiles of NLD loads each are still in flight
+// (ahead = tiles issued after the one needed next, 0 <= ahead <= MAXA).
+template <int NLD, int MAXA>
+__device__ __forceinline__ void wait_tiles(int ahead) {
+  if constexpr (MAXA <= 0) {
+    wait_vmem<0>();
+  } else {
+    if (ahead >= MAXA) wait_vmem<MAXA * NLD>();
+    else wait_tiles<NLD, MAXA - 1>(ahead);
+  }
+}
+
+// Pins x to this point of the program: the compiler must have x here (it
+// waits for the load that produced it here, once, instead of at a first use
+// inside a tile loop, where the wait would also drain a prefetch ring), and
+// cannot sink the computation of x past this point.
+template <typename T>
+__device__ __forceinline__ void settle(T& x) {
+  asm volatile("" : "+v"(x));
+}
+
 // 2^x on the transcendental unit (v_exp_f32); -inf gives 0.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 

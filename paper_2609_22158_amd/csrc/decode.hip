@@ -3,10 +3,11 @@
 // accumulation (the consumer of the compacted cache, Sec. 3).
 //
 // decode_mfma_kernel: one workgroup per (layer, KV head, sequence, split of
-// 512 retained rows) serves all G <= 16 query heads of the KV head, so K and V
-// are read once: q . k for the whole query group on MFMA, an exact online
-// softmax per head, p V in fp32 on the vector units; decode_combine_kernel
-// merges the splits. decode_simple_kernel serves groups wider than 16 heads.
+// 512 or 1024 retained rows) serves all G <= 16 query heads of the KV head, so K and V
+// are read once: q . k and p V for the whole query group on MFMA with an
+// exact online softmax per head between them, several 16-row tiles in flight
+// per wave; decode_combine_kernel merges the splits. decode_simple_kernel
+// serves groups wider than 16 heads.
 #include "common.h"
 #include "internal.h"
 
@@ -14,6 +15,7 @@
 
 #include <algorithm>
 #include <type_traits>
+#include <utility>
 
 namespace stepkv {
 namespace {
@@ -97,25 +99,11 @@ __global__ __launch_bounds__(kThreads) void decode_simple_kernel(DecodeArgs a) {
 }
 
 
-#ifndef STEPKV_DECODE_SPLIT_ROWS
-#define STEPKV_DECODE_SPLIT_ROWS 512
-#endif
-constexpr int kSplitRows = STEPKV_DECODE_SPLIT_ROWS;  // retained rows per workgroup
 
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ void unpack8(const u32x4_t& w, float (&f)[8]) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    f[2 * i] = __uint_as_float(w[i] << 16);
-    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-  }
-}
-
-// Row splits of sequence s: ceil(R_s / kSplitRows).
+// Row splits of sequence s: ceil(R_s / split_rows).
 __device__ __forceinline__ int splits_of(const DecodeArgs& a, int s) {
   int r0;
-  return (rows_of(a, s, r0) + kSplitRows - 1) / kSplitRows;
+  return (rows_of(a, s, r0) + a.split_rows - 1) / a.split_rows;
 }
 
 // The sequence holding global split gs, and the first global split of that
@@ -151,22 +139,32 @@ __device__ __forceinline__ void locate_split(const DecodeArgs& a, int gs, int& s
 typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
 
-// One workgroup per (layer, KV head, sequence, split of kSplitRows retained
-// rows); each wave takes a quarter of the split in tiles of 16 rows and keeps
-// its own online-softmax state.
-//  - S = K_tile Q^T on v_mfma_f32_16x16x32_bf16: A = 16 key rows, B = the
-//    group's query heads (16 columns, heads past G are zero). The d axis is
-//    permuted so that lane l reads 2D/4 contiguous bytes of row l % 16 (the
-//    query uses the same permutation). Lane l then holds head l % 16 for rows
-//    4 (l / 16) + 0..3 of the tile.
-//  - Softmax per head in that layout: the tile maximum over the four lane
-//    groups, a reference per head that moves only when a logit passes it by
-//    more than 2^kSlack (so p <= 2^kSlack and rescaling is rare), p = 2^(x - m).
-//  - p goes through a per-wave LDS tile to the value lanes: 8 dims of one row
-//    per lane (coalesced 16-byte loads), o[g][:] += p[g][row] * v[row][:] in
-//    fp32 for the GM heads.
+// One workgroup per (layer, KV head, sequence, split of split_rows retained
+// rows); each wave takes a quarter of the split in tiles of 16 rows, keeps its
+// own online-softmax state and its own ring of NST tiles in flight: K to
+// registers, V straight to LDS (global_load_lds), tile t + NST - 1 issued
+// before tile t is computed. Both products run on MFMA with the query group as
+// 16 columns (heads past G are zero):
+//  - S = K_tile Q^T on v_mfma_f32_16x16x32_bf16: A = the 16 key rows, B = the
+//    query heads. Lane group g = l / 16 reads 16-byte pieces 4 ks + g of its
+//    row for k-step ks (64 contiguous bytes per row and load; the query takes
+//    the same d order). Lane l then holds head l % 16 for rows 4 g + 0..3.
+//  - Softmax per head in that layout: a reference per head that moves only
+//    when a logit passes it by more than 2^kSlack (so p <= 2^kSlack and
+//    rescaling is rare), p = 2^(x - m).
+//  - O += P V on v_mfma_f32_16x16x16_bf16: A = P as the lanes hold it (head
+//    l % 16, rows 4 g + 0..3), split into bf16 hi + lo parts (P to about
+//    2^-17 relative); B = 16 value columns of those rows, read from the LDS
+//    tile with the transposing read ds_read_b64_tr_b16. Lane l then holds
+//    heads 4 g + 0..3 of the 16 columns.
+// The V tile in LDS is row-major with the 32-byte pairs of row r XOR-swizzled
+// by swz(r), so that the 32 lanes of each transposing read hit distinct banks.
 // Waves merge in LDS; decode_combine_kernel merges the splits.
 constexpr float kSlack = 16.f;
+
+// Tiles per wave in the ring: one computed while the next is in flight (a
+// deeper ring costs occupancy and measured no faster).
+constexpr int kStages = 2;
 
 // Cross-lane exchanges on the vector unit (no LDS round trip): the value of
 // lane l ^ 16 and of lane l ^ 32 (gfx950 permlane swaps).
@@ -181,21 +179,69 @@ __device__ __forceinline__ float xor32(float x) {
                                                   false);
   return __uint_as_float(((threadIdx.x >> 5) & 1) ? r[0] : r[1]);
 }
-template <int D, int GM>
-__global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
-  constexpr int KS = D / 32;          // MFMA k-steps over d
-  constexpr int KQ = D / 4;           // d entries per lane group (q = lane / 16) and row
-  constexpr int LPR = D / 8;          // value lanes per row (8 dims each)
-  constexpr int RPL = kWave / LPR;    // value rows per load instruction
-  constexpr int VL = 16 / RPL;        // value loads per lane and tile
+
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+
+// f(integral_constant<int, 0>) ... f(integral_constant<int, N - 1>), unrolled.
+template <typename F, int... U>
+__device__ __forceinline__ void static_for_impl(F& f, std::integer_sequence<int, U...>) {
+  (f(std::integral_constant<int, U>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// XOR swizzle (in 32-byte pairs) of row r of a V tile: rows 8k .. 8k + 7 land
+// on distinct bank groups (D = 128: 8 pairs a row; D = 64: 4 pairs a row, two
+// rows per 256 bytes).
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  return D == 128 ? (r & 7) : ((r >> 1) & 3);
+}
+
+// Transposing LDS read at byte address addr + OFF. Issued as assembly so that
+// the compiler, which cannot tell the ring slots apart, puts no wait for the
+// whole ring's direct-to-LDS loads in front of it; completion is awaited with
+// tr_settle.
+template <int OFF>
+__device__ __forceinline__ i16x4_t lds_read_tr(uint32_t addr) {
+  i16x4_t v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF) : "memory");
+  return v;
+}
+
+template <int N>
+__device__ __forceinline__ void tr_settle(i16x4_t (&f)[N]) {
+  static_assert(N == 4 || N == 8, "value blocks");
+  if constexpr (N == 4) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]));
+  } else {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5]),
+                   "+v"(f[6]), "+v"(f[7]));
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3)))
+void decode_mfma_kernel(DecodeArgs a) {
+  constexpr int KS = D / 32;         // 16-byte K pieces per lane and row = S k-steps
+  constexpr int PR = D / 8;          // 16-byte pieces per row
+  constexpr int RPI = kWave / PR;    // V rows per direct-to-LDS load
+  constexpr int VL = 16 / RPI;       // V loads per tile
+  constexpr int NLD = KS + VL;       // vector memory operations per tile and lane
+  constexpr int NB = D / 16;         // 16-column blocks of O
   constexpr int NW = kThreads / kWave;
-  constexpr int ST = D + 2;           // floats per head in a partial state: o[D], m, z
-  static_assert(GM % 4 == 0 && GM <= 16, "heads per group");
-  __shared__ __attribute__((aligned(16))) float ptile[NW][16][16];  // p[row][head] per wave
-  __shared__ __attribute__((aligned(16))) float fscale[NW][16];     // rescale factors per head
-  __shared__ float wstate[NW][GM][ST];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int q = lane >> 4, c16 = lane & 15;
+  constexpr int ST = D + 2;          // floats per head in a partial state: o[D], m, z
+  constexpr int TB = 16 * D * 2;     // bytes of a V tile
+  constexpr int kRingBytes = NW * kStages * TB, kStateBytes = NW * 16 * ST * 4;
+  // the V rings during the sweep; the per-wave states [NW][16][ST] after it
+  __shared__ __attribute__((aligned(16)))
+  uint8_t smem[kRingBytes > kStateBytes ? kRingBytes : kStateBytes];
+  __shared__ __attribute__((aligned(16))) float fscale[NW][16];  // rescale factors
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+  const int g4 = lane >> 4, c16 = lane & 15;
   const int lh = blockIdx.x / a.total_splits;
   const int gs = blockIdx.x - lh * a.total_splits;
   int s, first;
@@ -206,132 +252,142 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
   const int l = lh / a.Hkv, h = lh - l * a.Hkv;
   int r0;
   const int R = rows_of(a, s, r0);
-  constexpr int kWaveRows = kSplitRows / NW;
-  const int w0 = j * kSplitRows + wave * kWaveRows;  // this wave's rows [w0, w1)
-  const int w1 = min(R, w0 + kWaveRows);
-  // query heads as the B operand: head c16, d = q KQ + 8 ks + 0..7
+  const int wave_rows = a.split_rows / NW;
+  const int w0 = j * a.split_rows + wave * wave_rows;  // this wave's rows [w0, w1)
+  const int w1 = min(R, w0 + wave_rows);
+  const int ntiles = w1 > w0 ? (w1 - w0 + 15) / 16 : 0;
+  // query heads as the B operand of S: head c16, d piece 4 ks + g4
   bf16x8_t qb[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     qb[ks] = bf16x8_t{};
     if (c16 < a.G)
       qb[ks] = *reinterpret_cast<const bf16x8_t*>(
-          a.q + (((size_t)l * a.S + s) * a.Hq + h * a.G + c16) * D + q * KQ + 8 * ks);
+          a.q + (((size_t)l * a.S + s) * a.Hq + h * a.G + c16) * D + 8 * (4 * ks + g4));
   }
   const float cl2 = a.scale * 1.44269504088896341f;  // logits in the log2 domain
   float m_ref = -INFINITY;  // reference of head c16 (the same in the four lane groups)
   float zp = 0.f;           // this lane's share of head c16's sum
-  float o[GM][8];
+  f32x4_t o[NB];            // O[head 4 g4 + i][16 nb + c16]
 #pragma unroll
-  for (int g = 0; g < GM; ++g)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) o[g][i] = 0.f;
+  for (int nb = 0; nb < NB; ++nb) o[nb] = f32x4_t{};
   const uint16_t* kb = a.k + ((size_t)lh * a.out_rows + r0) * D;
   const uint16_t* vb = a.v + ((size_t)lh * a.out_rows + r0) * D;
-  const int vrow = lane / LPR, vcol = 8 * (lane % LPR);
-  // the tile at row t: K as the MFMA A operand, V as 8 dims of a row per lane;
-  // rows past the end re-read the last one
-  auto load = [&](int t, bf16x8_t (&ka)[KS], u32x4_t (&vw)[VL]) __attribute__((always_inline)) {
-    const int rk = min(t + c16, w1 - 1);
+  uint8_t* ring = smem + wave * (kStages * TB);  // this wave's V tiles
+  // direct-to-LDS loads: lane l fills LDS piece l % PR of row i RPI + l / PR,
+  // which holds global piece (l % PR) ^ 2 swz(row)
+  const int vrow = lane / PR;
+  const int vpiece = lane % PR;
+  // transposing reads: lane (g4, c16) supplies row 4 g4 + c16 / 4, columns
+  // 16 nb + 4 (c16 % 4) .. + 3 (8 bytes of pair nb ^ swz(row))
+  uint32_t tr_addr[NB];
+  {
+    const int r = 4 * g4 + (c16 >> 2);
+    const uint32_t base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
+                              (__attribute__((address_space(3))) uint8_t*)ring)) +
+                          r * (2 * D) + 8 * (c16 & 3);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) tr_addr[nb] = base + 32 * (nb ^ swz<D>(r));
+  }
+  bf16x8_t ka[kStages][KS];
+  auto issue = [&](int tt, auto slot_c) __attribute__((always_inline)) {
+    constexpr int slot = decltype(slot_c)::value;
+    const int t = w0 + 16 * tt;
+    const int rk = min(t + c16, w1 - 1);  // rows past the end re-read the last one
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      ka[ks] = __builtin_nontemporal_load(
-          reinterpret_cast<const bf16x8_t*>(kb + (size_t)rk * D + q * KQ + 8 * ks));
+      ka[slot][ks] = __builtin_nontemporal_load(
+          reinterpret_cast<const bf16x8_t*>(kb + (size_t)rk * D + 8 * (4 * ks + g4)));
 #pragma unroll
     for (int i = 0; i < VL; ++i) {
-      const int rv = min(t + i * RPL + vrow, w1 - 1);
-      vw[i] = __builtin_nontemporal_load(
-          reinterpret_cast<const u32x4_t*>(vb + (size_t)rv * D + vcol));
+      const int r = i * RPI + vrow;
+      const int rv = min(t + r, w1 - 1);
+      __builtin_amdgcn_global_load_lds(
+          static_cast<const void*>(vb + (size_t)rv * D + 8 * (vpiece ^ (2 * swz<D>(r)))),
+          (__attribute__((address_space(3))) void*)(ring + slot * TB + i * (16 * kWave)), 16, 0,
+          0);
     }
   };
-  for (int t = w0; t < w1; t += 16) {  // wave-uniform loop
-    bf16x8_t ka[KS];
-    u32x4_t vw[VL];
-    load(t, ka, vw);
-    // every load of the tile is in flight before the first wait (one memory
-    // round trip per tile, not one for K and another for V)
-    __builtin_amdgcn_sched_barrier(0);
+  auto compute = [&](int tt, auto slot_c) __attribute__((always_inline)) {
+    constexpr int slot = decltype(slot_c)::value;
+    const int t = w0 + 16 * tt;
+    wait_tiles<NLD, kStages - 1>(min(kStages - 1, ntiles - 1 - tt));
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) settle(ka[slot][ks]);
+    // V blocks of this tile from LDS while S runs on the matrix cores
+    i16x4_t vbop[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) vbop[nb] = lds_read_tr<slot * TB>(tr_addr[nb]);
     f32x4_t acc = f32x4_t{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[ks], qb[ks], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[slot][ks], qb[ks], acc, 0, 0, 0);
     float x[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) x[i] = t + 4 * q + i < w1 ? acc[i] * cl2 : -INFINITY;
+    for (int i = 0; i < 4; ++i) x[i] = t + 4 * g4 + i < w1 ? acc[i] * cl2 : -INFINITY;
     float tmax = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
     // -inf never moves the reference; the first finite tile does
     if (__builtin_amdgcn_ballot_w64(tmax > m_ref + kSlack) != 0) {  // wave-uniform, rare
-      // the tile maximum of each head over its four lane groups
-      tmax = fmaxf(tmax, xor16(tmax));
+      tmax = fmaxf(tmax, xor16(tmax));  // the tile maximum of each head
       tmax = fmaxf(tmax, xor32(tmax));
       const bool move = tmax > m_ref + kSlack;  // the same in the four lane groups of a head
       const float m_new = move ? tmax : m_ref;
       const float f = m_ref == -INFINITY ? 0.f : fast_exp2(m_ref - m_new);
       zp *= f;
       m_ref = m_new;
-      if (q == 0) fscale[wave][c16] = f;
+      if (g4 == 0) fscale[wave][c16] = f;
       __builtin_amdgcn_wave_barrier();
-      float fs[GM];
+      const float4 f4 = *reinterpret_cast<const float4*>(&fscale[wave][4 * g4]);  // heads 4 g4 + i
 #pragma unroll
-      for (int g = 0; g < GM; g += 4) {
-        const float4 v4 = *reinterpret_cast<const float4*>(&fscale[wave][g]);
-        fs[g] = v4.x;
-        fs[g + 1] = v4.y;
-        fs[g + 2] = v4.z;
-        fs[g + 3] = v4.w;
+      for (int nb = 0; nb < NB; ++nb) {
+        o[nb][0] *= f4.x;
+        o[nb][1] *= f4.y;
+        o[nb][2] *= f4.z;
+        o[nb][3] *= f4.w;
       }
-#pragma unroll
-      for (int g = 0; g < GM; ++g)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) o[g][i] *= fs[g];
     }
-    float p[4];
+    i16x4_t ph, pl;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      p[i] = x[i] == -INFINITY ? 0.f : fast_exp2(x[i] - m_ref);
-      zp += p[i];
-      ptile[wave][4 * q + i][c16] = p[i];
+      const float pi = x[i] == -INFINITY ? 0.f : fast_exp2(x[i] - m_ref);
+      zp += pi;
+      const __bf16 hi = (__bf16)pi;
+      ph[i] = __builtin_bit_cast(short, hi);
+      pl[i] = __builtin_bit_cast(short, (__bf16)(pi - (float)hi));
     }
-    __builtin_amdgcn_wave_barrier();
+    tr_settle(vbop);
 #pragma unroll
-    for (int i = 0; i < VL; ++i) {
-      const int rr = i * RPL + vrow;  // row of the tile
-      float pr[GM];
-#pragma unroll
-      for (int g = 0; g < GM; g += 4) {
-        const float4 v4 = *reinterpret_cast<const float4*>(&ptile[wave][rr][g]);
-        pr[g] = v4.x;
-        pr[g + 1] = v4.y;
-        pr[g + 2] = v4.z;
-        pr[g + 3] = v4.w;
-      }
-      float v[8];
-      unpack8(vw[i], v);
-#pragma unroll
-      for (int g = 0; g < GM; ++g)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[g][e] = fmaf(pr[g], v[e], o[g][e]);
+    for (int nb = 0; nb < NB; ++nb) {
+      o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ph, vbop[nb], o[nb], 0, 0, 0);
+      o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pl, vbop[nb], o[nb], 0, 0, 0);
     }
-    __builtin_amdgcn_wave_barrier();  // the tile's p reads precede the next tile's writes
+  };
+  // the ring: tiles 0 .. kStages - 2 first, then tile tt + kStages - 1 (into
+  // the slot tile tt - 1 left) before tile tt is computed
+  static_for<kStages - 1>([&](auto u_c) __attribute__((always_inline)) {
+    if (decltype(u_c)::value < ntiles) issue(decltype(u_c)::value, u_c);
+  });
+  for (int t0 = 0; t0 < ntiles; t0 += kStages) {  // wave-uniform loop
+    static_for<kStages>([&](auto u_c) __attribute__((always_inline)) {
+      constexpr int u = decltype(u_c)::value;
+      const int tt = t0 + u;
+      if (tt >= ntiles) return;
+      if (tt + kStages - 1 < ntiles)
+        issue(tt + kStages - 1, std::integral_constant<int, (u + kStages - 1) % kStages>{});
+      compute(tt, u_c);
+    });
   }
-  // this wave's sums: z over the four lane groups, o over the row groups of the value lanes
+  // this wave's sums: z over the four lane groups of each head
   zp += xor16(zp);
   zp += xor32(zp);
+  __syncthreads();  // the states overwrite the V rings of every wave
+  auto wstate = reinterpret_cast<float(*)[16][ST]>(smem);
 #pragma unroll
-  for (int off = LPR; off < kWave; off <<= 1)
+  for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-    for (int g = 0; g < GM; ++g)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[g][i] += __shfl_xor(o[g][i], off, kWave);
-  if (lane < LPR) {
-#pragma unroll
-    for (int g = 0; g < GM; ++g) {
-      if (g >= a.G) break;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) wstate[wave][g][vcol + i] = o[g][i];
-    }
-  }
-  if (q == 0 && c16 < a.G) {
+    for (int i = 0; i < 4; ++i)
+      if (4 * g4 + i < a.G) wstate[wave][4 * g4 + i][16 * nb + c16] = o[nb][i];
+  if (g4 == 0 && c16 < a.G) {
     wstate[wave][c16][D] = m_ref;
     wstate[wave][c16][D + 1] = zp;
   }
@@ -344,9 +400,9 @@ __global__ __launch_bounds__(kThreads) void decode_mfma_kernel(DecodeArgs a) {
       const float mw = wstate[w][g][D], zw = wstate[w][g][D + 1];
       const float mn = fmaxf(M, mw);
       if (mn == -INFINITY) continue;
-      const float x = fast_exp2(M - mn), y = fast_exp2(mw - mn);
-      Z = Z * x + zw * y;
-      O = O * x + wstate[w][g][dd] * y;
+      const float xa = fast_exp2(M - mn), ya = fast_exp2(mw - mn);
+      Z = Z * xa + zw * ya;
+      O = O * xa + wstate[w][g][dd] * ya;
       M = mn;
     }
     float* part = a.partial + (((size_t)lh * a.total_splits + gs) * a.G + g) * ST;
@@ -413,16 +469,25 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(DecodeArgs a) {
 
 }  // namespace
 
-// A bound of sum_s ceil(R_s / kSplitRows) from what the host knows: R_s <=
+// 1024 rows per split when the cache fills the chip's resident workgroups
+// (256 CUs x 3) at least twice over with them, else 512: longer splits spend
+// less of each workgroup's life on its start and merge, shorter ones keep a
+// small cache spread over every CU.
+int decode_split_rows(int L, int Hkv, int out_rows) {
+  constexpr int64_t kResident = 256 * 3;
+  return (int64_t)L * Hkv * (out_rows / 1024) >= 2 * kResident ? 1024 : 512;
+}
+
+// A bound of sum_s ceil(R_s / split_rows) from what the host knows: R_s <=
 // min(N_s, out_rows), and sum_s R_s <= out_rows gives at most
-// floor(out_rows / kSplitRows) + S splits.
-int decode_total_splits(const int32_t* cu_seqlens_host, int S, int out_rows) {
+// floor(out_rows / split_rows) + S splits.
+int decode_total_splits(const int32_t* cu_seqlens_host, int S, int out_rows, int split_rows) {
   int64_t acc = 0;
   for (int s = 0; s < S; ++s) {
     const int n = std::min(cu_seqlens_host[s + 1] - cu_seqlens_host[s], out_rows);
-    acc += (n + kSplitRows - 1) / kSplitRows;
+    acc += (n + split_rows - 1) / split_rows;
   }
-  return (int)std::min<int64_t>(acc, (int64_t)(out_rows / kSplitRows) + S);
+  return (int)std::min<int64_t>(acc, (int64_t)(out_rows / split_rows) + S);
 }
 
 size_t decode_partial_floats(const DecodeArgs& a) {
@@ -441,24 +506,10 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
   }
   if (a.total_splits > 0) {
     const dim3 grid((unsigned)(a.L * a.Hkv) * (unsigned)a.total_splits);
-    auto go = [&](auto d_c, auto gm_c) {
-      constexpr int Dd = decltype(d_c)::value, GMm = decltype(gm_c)::value;
-      hipLaunchKernelGGL((decode_mfma_kernel<Dd, GMm>), grid, dim3(kThreads), 0, st, a);
-    };
-    using I128 = std::integral_constant<int, 128>;
-    using I64 = std::integral_constant<int, 64>;
-    using G4 = std::integral_constant<int, 4>;
-    using G8 = std::integral_constant<int, 8>;
-    using G16 = std::integral_constant<int, 16>;
-    if (a.d == 128) {
-      if (a.G <= 4) go(I128{}, G4{});
-      else if (a.G <= 8) go(I128{}, G8{});
-      else go(I128{}, G16{});
-    } else {
-      if (a.G <= 4) go(I64{}, G4{});
-      else if (a.G <= 8) go(I64{}, G8{});
-      else go(I64{}, G16{});
-    }
+    if (a.d == 128)
+      hipLaunchKernelGGL(decode_mfma_kernel<128>, grid, dim3(kThreads), 0, st, a);
+    else
+      hipLaunchKernelGGL(decode_mfma_kernel<64>, grid, dim3(kThreads), 0, st, a);
   }
   const dim3 cgrid((unsigned)(a.L * a.S * a.Hq));
   if (a.d == 128)

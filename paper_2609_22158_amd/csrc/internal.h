@@ -129,11 +129,15 @@ struct DecodeArgs {
   float* partial;            // workspace: [L*Hkv][total_splits][G][d+2] (o, m, z)
   uint32_t* status;          // device status word (STEPKV_FLAG_*) or null
   int L, S, Hq, Hkv, G, d, out_rows, total_splits;
+  int split_rows;            // retained rows per workgroup of the split kernel
   float scale;
 };
-// Row splits of the split kernel for these sequence lengths and out_rows.
-int decode_total_splits(const int32_t* cu_seqlens_host, int S, int out_rows);
-// Floats of partial state the launch needs (0 for groups above 8 heads).
+// Rows per split for this cache size (512 or 1024).
+int decode_split_rows(int L, int Hkv, int out_rows);
+// Row splits of the split kernel (a host-side bound) for these sequence
+// lengths, out_rows and rows per split.
+int decode_total_splits(const int32_t* cu_seqlens_host, int S, int out_rows, int split_rows);
+// Floats of partial state the launch needs (0 for groups above 16 heads).
 size_t decode_partial_floats(const DecodeArgs& a);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t st);
 

@@ -41,23 +41,6 @@ __device__ __forceinline__ int tile_offset(int r, int p) {
   return r * (2 * D) + 16 * (p ^ swizzle<D>(r));
 }
 
-template <int N>
-__device__ __forceinline__ void wait_vmem() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// Wait until at most `ahead` tiles of NLD loads each are still in flight
-// (ahead = tiles issued after the one needed next, 0 <= ahead <= MAXA).
-template <int NLD, int MAXA>
-__device__ __forceinline__ void wait_tiles(int ahead) {
-  if constexpr (MAXA <= 0) {
-    wait_vmem<0>();
-  } else {
-    if (ahead >= MAXA) wait_vmem<MAXA * NLD>();
-    else wait_tiles<NLD, MAXA - 1>(ahead);
-  }
-}
-
 // K ring per workgroup: four 8 KiB tiles at W*G = 256 rows, four 16 KiB tiles
 // at 128 rows, two 32 KiB tiles at 64 rows; two workgroups per CU fit in LDS.
 #ifndef STEPKV_SAL_RING_BYTES
@@ -69,15 +52,6 @@ __device__ __forceinline__ void wait_tiles(int ahead) {
 #ifndef STEPKV_SAL_SYNC_TILES
 #define STEPKV_SAL_SYNC_TILES 2
 #endif
-
-// Pins x to this point of the program: the compiler must have x here (it
-// waits for the load that produced it here, once, instead of at a first use
-// inside the tile loop, where the wait would also drain the K prefetch ring),
-// and cannot sink the computation of x past this point.
-template <typename T>
-__device__ __forceinline__ void settle(T& x) {
-  asm volatile("" : "+v"(x));
-}
 
 // One 16-byte LDS read of the K ring at addr + OFF. Issued as assembly so
 // that the compiler, which cannot tell the ring slots apart, does not put a

@@ -198,11 +198,14 @@ def test_select_compact_decode_reject(lib):
 def test_decode_workspace_counts_splits(lib):
     """The decode workspace holds one fp32 state (o[d], m, z) per (layer, KV head, split, head
     of the group); splits of 512 rows number min(sum_s ceil(min(N_s, out_rows) / 512),
-    floor(out_rows / 512) + S), the two bounds of sum_s ceil(R_s / 512) the host knows."""
+    floor(out_rows / 512) + S), the two bounds of sum_s ceil(R_s / 512) the host knows.
+    Splits are of 1024 rows instead once L * Hkv * floor(out_rows / 1024) >= 1536."""
     per_split = 2 * 2 * 4 * (128 + 2) * 4  # L * Hkv * G * (d + 2) floats
     for cu, out_rows, splits in [((0, 1000, 3000), 8, 2), ((0, 1000, 3000), 3000, 6),
                                  ((0, 20000, 40000), 1026, 4), ((0, 20000, 40000), 1024, 4),
-                                 ((0, 20000, 40000), 1023, 3)]:
+                                 ((0, 20000, 40000), 1023, 3),
+                                 ((0, 400000, 800000), 393215, 769),  # 4 * 383 < 1536
+                                 ((0, 400000, 800000), 400000, 392)]:  # 4 * 390: 1024 rows
         pb = _problem(cu=cu)
         assert lib.stepkv_decode_workspace_bytes(ctypes.byref(pb), out_rows) == splits * per_split
 

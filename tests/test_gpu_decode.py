@@ -7,8 +7,9 @@ ragged retained counts (0, 1, and several 256-row splits) and query groups of 1,
 per-head kernel), one case whose logits spread over ~100 nats, so the running
 reference of each head moves in the middle of a split, one whose sequences are far
 longer than what they retain (the split count then comes from out_rows, and here every
-split that bound allows holds rows), and one whose out_rows cuts the last sequences
-short (rows at or past out_rows are not read)."""
+split that bound allows holds rows), one whose out_rows cuts the last sequences
+short (rows at or past out_rows are not read), and one large enough for splits of 1024
+rows instead of 512."""
 import math
 import zlib
 
@@ -39,6 +40,8 @@ CASES = {
     "g8_d128_tight": (1, 16, 2, 128, [513, 513, 513, 513], 0, 3.0, 20000),
     # out_rows = 950: the second sequence keeps 250 rows, the third none
     "g4_d128_short": (1, 8, 2, 128, [700, 600, 300], -650, 3.0),
+    # L * Hkv * floor(out_rows / 1024) = 1632 >= 2 * 768: splits of 1024 rows
+    "g2_d64_long": (2, 16, 8, 64, [30000, 25000, 1, 50000], 0, 3.0),
 }
 
 
