@@ -36,6 +36,8 @@
  *  - bf16 tensors hold raw bfloat16 values (2 bytes each).
  *  - Arguments are validated on the host before anything is launched; a
  *    failed validation returns an error code and launches nothing.
+ *  - Outputs do not overlap inputs. Where a call takes both, scores and
+ *    saliency are checked: overlapping ones are EINVAL.
  *  - No C++ exception crosses this interface.
  *  - Conditions only the device can see (a step id out of range, a
  *    non-finite input, rows past out_rows) are reported through the
@@ -295,8 +297,12 @@ int stepkv_saliency_from_lse(const stepkv_problem* pb, const stepkv_params* prm,
  *   T_i = (1/k) sum_{|j-i| <= k/2} A_j [j prunable], zero padding, per sequence
  *   Th_i = T_i / max_{prunable} T  (0 when that max is 0)
  *   P_i  = alpha * Th_i + beta * S_{step_ids[i]};  protected: -inf
- * plus the optional per-step statistics (see stepkv_score). No workspace.
- * Errors: EINVAL, EUNSUPPORTED (pool window, stats step count), EHIP. */
+ * plus the optional per-step statistics (see stepkv_score). No workspace:
+ * without statistics, and with more (sequence, layer, KV head) rows than
+ * 256, each row is spread over workgroups of 2048 positions, which keep
+ * their partial maxima in the scores row until they overwrite it.
+ * Errors: EINVAL (also scores overlapping saliency), EUNSUPPORTED (pool
+ * window, stats step count), EHIP. */
 int stepkv_priority(const stepkv_problem* pb, const stepkv_params* prm, const float* saliency,
                     const int32_t* step_ids, const uint8_t* protected_mask,
                     const float* step_utility, float* scores, stepkv_step_stat* step_stats,

@@ -309,15 +309,24 @@ int run_priority(const stepkv_problem* pb, const stepkv_params* prm, const float
   fa.half = prm->pool_kernel / 2;
   fa.max_steps = std::max(max_steps_per_seq(pb), 1);
   fa.max_len = max_seqlen(pb);
+  fa.total_chunks = prio_chunks(pb->cu_seqlens_host, pb->num_seqs);
   fa.alpha = prm->alpha;
   fa.beta = prm->beta;
   return hip_status(launch_fuse(fa, st));
 }
 
+// The priority reads the saliency around each position while other
+// workgroups write scores (and keep partial results in the scores rows), so
+// the two arrays of `rows` x Ntot floats must not share memory.
 int check_priority_args(const stepkv_problem* pb, const int32_t* step_ids,
                         const uint8_t* protected_mask, const float* util, const float* scores,
-                        const stepkv_step_stat* stats) {
+                        const stepkv_step_stat* stats, const float* sal, size_t rows) {
   if (!step_ids || !protected_mask || !scores) return STEPKV_EINVAL;
+  if (sal) {
+    const uintptr_t n = sizeof(float) * rows * (size_t)pb->cu_seqlens_host[pb->num_seqs];
+    const uintptr_t a = reinterpret_cast<uintptr_t>(sal), b = reinterpret_cast<uintptr_t>(scores);
+    if (a < b + n && b < a + n) return STEPKV_EINVAL;
+  }
   if (!util && pb->cu_steps_host[pb->num_seqs] > 0) return STEPKV_EINVAL;
   if (stats && max_steps_per_seq(pb) > STEPKV_MAX_STEPS_STATS) return STEPKV_EUNSUPPORTED;
   return STEPKV_OK;
@@ -403,7 +412,8 @@ int stepkv_priority(const stepkv_problem* pb, const stepkv_params* prm, const fl
   if (rc == STEPKV_OK) rc = check_params(pb, prm);
   if (rc != STEPKV_OK) return rc;
   if (!saliency) return STEPKV_EINVAL;
-  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats);
+  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats,
+                           saliency, (size_t)pb->num_layers * pb->num_kv_heads);
   if (rc != STEPKV_OK) return rc;
   if (pb->cu_seqlens_host[pb->num_seqs] == 0) return STEPKV_OK;
   return run_priority(pb, prm, saliency, step_ids, protected_mask, step_utility, scores,
@@ -418,7 +428,8 @@ int stepkv_score(const stepkv_problem* pb, const stepkv_params* prm, const void*
   if (rc == STEPKV_OK) rc = check_params(pb, prm);
   if (rc != STEPKV_OK) return rc;
   if (!q_win || !k) return STEPKV_EINVAL;
-  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats);
+  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats,
+                           saliency, (size_t)pb->num_layers * pb->num_kv_heads);
   if (rc != STEPKV_OK) return rc;
   const WsLayout w = layout(pb, plan_saliency(pb));
   if (!workspace || ws_bytes < w.total || !aligned(workspace)) return STEPKV_EWORKSPACE;
@@ -441,7 +452,8 @@ int stepkv_score_noalloc(const stepkv_problem* pb, const stepkv_params* prm, con
   if (rc == STEPKV_OK) rc = check_params(pb, prm);
   if (rc != STEPKV_OK) return rc;
   if (!q_win || !k || !saliency) return STEPKV_EINVAL;
-  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats);
+  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats,
+                           saliency, (size_t)pb->num_layers * pb->num_kv_heads);
   if (rc != STEPKV_OK) return rc;
   // the sweeps' workspace (everything but the saliency buffer, which the caller passes)
   if (layout(pb, plan_saliency(pb)).sal > kStaticScratchBytes) return STEPKV_ESCRATCH;
@@ -492,7 +504,8 @@ int stepkv_score_from_lse(const stepkv_problem* pb, const stepkv_params* prm, co
   if (rc == STEPKV_OK) rc = check_params(pb, prm);
   if (rc != STEPKV_OK) return rc;
   if (!q_win || !k || !lse_win) return STEPKV_EINVAL;
-  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats);
+  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats,
+                           saliency, (size_t)pb->num_layers * pb->num_kv_heads);
   if (rc != STEPKV_OK) return rc;
   const WsLayout w = layout(pb, plan_saliency(pb));
   if (!workspace || ws_bytes < w.total || !aligned(workspace)) return STEPKV_EWORKSPACE;
@@ -521,7 +534,8 @@ int stepkv_score_shared(const stepkv_problem* pb, const stepkv_params* prm, cons
   if (rc == STEPKV_OK) rc = check_params(pb, prm);
   if (rc != STEPKV_OK) return rc;
   if (!q_win || !k || last_layers < 1) return STEPKV_EINVAL;
-  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats);
+  rc = check_priority_args(pb, step_ids, protected_mask, step_utility, scores, step_stats,
+                           saliency, 1);
   if (rc != STEPKV_OK) return rc;
   const int n = shared_layers(pb, last_layers);
   const SharedLayout w = shared_layout(pb, n);

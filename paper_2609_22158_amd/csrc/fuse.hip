@@ -1,5 +1,7 @@
-// Pooling, normalisation and step-utility fusion (Sec. 5.2, eq. token-priority)
-// with segmented per-step statistics, one workgroup per (sequence, head):
+// Pooling, normalisation and step-utility fusion (Sec. 5.2, eq. token-priority).
+// Without step statistics and with more (sequence, head) rows than CUs, each
+// row is spread over workgroups of 2048 positions (prio_chunk_*). Otherwise
+// one workgroup per (sequence, head):
 //   U_i  = sum_{|j-i| <= half} A_j [j prunable]     (k * T_i; zero padded)
 //   Th_i = U_i / max_{prunable} U                   (the 1/k cancels)
 //   P_i  = alpha * Th_i + beta * S[step_ids[i]]     (prunable; -inf if protected)
@@ -492,6 +494,184 @@ __global__ __launch_bounds__(kShChunk) void shared_fuse_kernel(SharedPrioArgs a)
   report_flags(a.status, bad);
 }
 
+// Per-head priority without step statistics: each (layer, KV head) row is
+// spread over workgroups of kPrChunk positions instead of one workgroup per
+// (sequence, row), in three launches. The chunk maxima live in the scores
+// row itself, at each chunk's first position, until the last launch
+// overwrites them:
+//   prio_chunk_max_kernel  pools its chunk, writes the chunk's maximum of the
+//                          pooled prunable values at the chunk's first position
+//   prio_row_max_kernel    per (sequence, row): the maximum over its chunks,
+//                          written back to every chunk's first position
+//   prio_chunk_fuse_kernel reads that maximum from its own chunk's first
+//                          position (before anyone writes there), pools again
+//                          and writes P
+// Pooling adds the window left to right from its first position, as
+// fuse_batched_kernel does, so U, its maximum and P agree with it bit for bit.
+constexpr int kPrThreads = 256;
+constexpr int kPrChunk = 2048;  // positions per workgroup, 8 per thread
+
+// Sequence s and chunk c of global chunk g (chunks of the sequences in
+// order): a wave-wide prefix over 64 sequences at a time, in every wave.
+__device__ __forceinline__ void locate_chunk(const int32_t* __restrict__ cu_seqlens, int S, int g,
+                                             int& s_out, int& c_out) {
+  const int lane = threadIdx.x & 63;
+  int base = 0;
+  for (int s0 = 0; s0 < S; s0 += kWave) {
+    const int sq = s0 + lane;
+    const int cnt = sq < S ? (cu_seqlens[sq + 1] - cu_seqlens[sq] + kPrChunk - 1) / kPrChunk : 0;
+    int incl = cnt;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int o = __shfl_up(incl, off, kWave);
+      if (lane >= off) incl += o;
+    }
+    const int total = __shfl(incl, kWave - 1, kWave);
+    if (g < base + total) {
+      const int first = __builtin_ctzll(ballot(base + incl > g));
+      s_out = s0 + first;
+      c_out = g - base - __shfl(incl - cnt, first, kWave);
+      return;
+    }
+    base += total;
+  }
+  s_out = -1;  // not reached for g below the chunk count
+  c_out = 0;
+}
+
+// am[e] = A at position p0 - half + e of the row's sequence when that
+// position exists and is prunable, else 0; e < kPrChunk + 2 half. Every load
+// of the chunk is issued before the first LDS write.
+__device__ __forceinline__ void prio_stage(const FuseArgs& a, const float* __restrict__ A,
+                                           const uint8_t* __restrict__ prot, int ns, int p0,
+                                           float* am) {
+  constexpr int J = kPrChunk / kPrThreads;
+  const int tid = threadIdx.x;
+  float v[J + 1];
+  uint32_t pr[J + 1];
+#pragma unroll
+  for (int j = 0; j <= J; ++j) {  // slot J: the 2 half halo positions past the chunk
+    const int e = tid + kPrThreads * j;
+    const int p = min(max(p0 - a.half + e, 0), max(ns - 1, 0));
+    v[j] = A[p];
+    pr[j] = prot[p];
+  }
+#pragma unroll
+  for (int j = 0; j <= J; ++j) {
+    const int e = tid + kPrThreads * j;
+    const int p = p0 - a.half + e;
+    if (j < J || e < kPrChunk + 2 * a.half)
+      am[e] = p >= 0 && p < ns && pr[j] == 0 ? v[j] : 0.f;
+  }
+}
+
+// U at position p0 + e (e < kPrChunk) from the stage: the 2 half + 1 values
+// around it, added left to right.
+template <int HALF>
+__device__ __forceinline__ float prio_pool(const float* am, int e, int half) {
+  float acc = 0.f;
+  if constexpr (HALF >= 0) {
+#pragma unroll
+    for (int o = 0; o <= 2 * HALF; ++o) acc += am[e + o];
+  } else {
+    for (int o = 0; o <= 2 * half; ++o) acc += am[e + o];
+  }
+  return acc;
+}
+
+template <int HALF>
+__global__ __launch_bounds__(kPrThreads) void prio_chunk_max_kernel(FuseArgs a) {
+  __shared__ float am[kPrChunk + 2 * kMaxHalf];
+  __shared__ float wred[kPrThreads / kWave];
+  const int lh = blockIdx.x / a.total_chunks, g = blockIdx.x - lh * a.total_chunks;
+  int s, c;
+  locate_chunk(a.cu_seqlens, a.S, g, s, c);
+  s = uniform(s);
+  if (s < 0) return;
+  const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
+  const int p0 = uniform(c) * kPrChunk;
+  const float* A = a.sal + (size_t)lh * a.ntot + seq0;
+  const uint8_t* prot = a.prot + seq0;
+  constexpr int J = kPrChunk / kPrThreads;
+  uint32_t pf[J];  // protected flags of this thread's positions
+#pragma unroll
+  for (int r = 0; r < J; ++r) pf[r] = prot[min(p0 + (int)threadIdx.x + kPrThreads * r, ns - 1)];
+  prio_stage(a, A, prot, ns, p0, am);
+  __syncthreads();
+  float m = 0.f;  // U >= 0
+#pragma unroll
+  for (int r = 0; r < J; ++r) {
+    const int e = threadIdx.x + kPrThreads * r;
+    if (p0 + e < ns && pf[r] == 0) m = fmaxf(m, prio_pool<HALF>(am, e, a.half));
+  }
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) wred[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float mm = 0.f;
+    for (int w = 0; w < kPrThreads / kWave; ++w) mm = fmaxf(mm, wred[w]);
+    a.scores[(size_t)lh * a.ntot + seq0 + p0] = mm;
+  }
+}
+
+__global__ __launch_bounds__(kWave) void prio_row_max_kernel(FuseArgs a) {
+  const int lh = blockIdx.x / a.S, s = blockIdx.x - lh * a.S;
+  const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
+  const int nch = (ns + kPrChunk - 1) / kPrChunk;
+  float* row = a.scores + (size_t)lh * a.ntot + seq0;
+  float m = 0.f;
+  for (int c = threadIdx.x; c < nch; c += kWave) m = fmaxf(m, row[(size_t)c * kPrChunk]);
+  m = wave_max(m);
+  for (int c = threadIdx.x; c < nch; c += kWave) row[(size_t)c * kPrChunk] = m;
+}
+
+template <int HALF, bool FLAGS>
+__global__ __launch_bounds__(kPrThreads) void prio_chunk_fuse_kernel(FuseArgs a) {
+  __shared__ float am[kPrChunk + 2 * kMaxHalf];
+  const int lh = blockIdx.x / a.total_chunks, g = blockIdx.x - lh * a.total_chunks;
+  int s, c;
+  locate_chunk(a.cu_seqlens, a.S, g, s, c);
+  s = uniform(s);
+  if (s < 0) return;
+  const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
+  const int p0 = uniform(c) * kPrChunk;
+  const float* A = a.sal + (size_t)lh * a.ntot + seq0;
+  const uint8_t* prot = a.prot + seq0;
+  const int32_t* sid = a.step_ids + seq0;
+  float* out = a.scores + (size_t)lh * a.ntot + seq0;
+  const float M = out[p0];  // the row's maximum; read before the barrier below
+  const int st0 = a.cu_steps[s], nsteps = a.cu_steps[s + 1] - st0;
+  constexpr int J = kPrChunk / kPrThreads;
+  int32_t kv[J];  // step ids and protected flags of this thread's positions
+  uint32_t pf[J];
+#pragma unroll
+  for (int r = 0; r < J; ++r) {
+    const int p = min(p0 + (int)threadIdx.x + kPrThreads * r, ns - 1);
+    kv[r] = sid[p];
+    pf[r] = prot[p];
+  }
+  prio_stage(a, A, prot, ns, p0, am);
+  __syncthreads();  // every thread has M before position p0 takes its P
+  const float inv = M > 0.f ? 1.0f / M : 0.f;
+  uint32_t bad = 0u;
+#pragma unroll
+  for (int r = 0; r < J; ++r) {
+    const int e = threadIdx.x + kPrThreads * r, p = p0 + e;
+    if (p < ns) {
+      const bool pr = pf[r] == 0;
+      const int kk = kv[r];
+      const bool ok = pr && kk >= 0 && kk < nsteps;
+      const float th = prio_pool<HALF>(am, e, a.half) * inv;
+      const float util = ok ? a.util[st0 + kk] : 0.f;
+      const float pv = pr ? fmaf(a.alpha, th, a.beta * util) : -INFINITY;
+      if (FLAGS)
+        bad |= (pr && !ok ? kFlagStepId : 0u) | (pr && !finite(pv) ? kFlagNonFinite : 0u);
+      out[p] = pv;
+    }
+  }
+  if (FLAGS) report_flags(a.status, bad);
+}
+
 }  // namespace
 
 int shared_chunks(const int32_t* cu_seqlens_host, int S) {
@@ -514,8 +694,43 @@ hipError_t launch_sum_heads(const float* sal, int heads, int ntot, float* out, h
   return hipGetLastError();
 }
 
+int prio_chunks(const int32_t* cu_seqlens_host, int S) {
+  int n = 0;
+  for (int t = 0; t < S; ++t) n += (cu_seqlens_host[t + 1] - cu_seqlens_host[t] + kPrChunk - 1) / kPrChunk;
+  return n;
+}
+
 hipError_t launch_fuse(const FuseArgs& a, hipStream_t st) {
   if (a.S * a.LH == 0) return hipSuccess;
+  // Without statistics, and when the (sequence, row) pairs outnumber the CUs
+  // (the per-sequence kernel runs one 1024-thread workgroup per CU, so it
+  // would take several rounds), each row is spread over workgroups of
+  // kPrChunk positions. Measured on MI355X: 28 layers x 4 heads x 16 ragged
+  // sequences 152 -> 118 us; with one round (32 x 8 rows of one 32k sequence)
+  // the per-sequence kernel stays ahead, 37 against 41 us.
+  if (!a.stats && a.S * a.LH > 256) {
+    if (a.total_chunks == 0) return hipSuccess;
+    const dim3 grid((unsigned)a.LH * (unsigned)a.total_chunks);
+    auto go = [&](auto half_c) {
+      constexpr int H = decltype(half_c)::value;
+      hipLaunchKernelGGL(prio_chunk_max_kernel<H>, grid, dim3(kPrThreads), 0, st, a);
+      hipLaunchKernelGGL(prio_row_max_kernel, dim3((unsigned)a.LH * (unsigned)a.S), dim3(kWave), 0,
+                         st, a);
+      if (a.status)
+        hipLaunchKernelGGL((prio_chunk_fuse_kernel<H, true>), grid, dim3(kPrThreads), 0, st, a);
+      else
+        hipLaunchKernelGGL((prio_chunk_fuse_kernel<H, false>), grid, dim3(kPrThreads), 0, st, a);
+    };
+    switch (a.half) {  // the usual pooling windows (1 .. 9) unrolled
+      case 0: go(std::integral_constant<int, 0>{}); break;
+      case 1: go(std::integral_constant<int, 1>{}); break;
+      case 2: go(std::integral_constant<int, 2>{}); break;
+      case 3: go(std::integral_constant<int, 3>{}); break;
+      case 4: go(std::integral_constant<int, 4>{}); break;
+      default: go(std::integral_constant<int, -1>{}); break;
+    }
+    return hipGetLastError();
+  }
   size_t dyn = (size_t)a.max_steps * 4;
   if (a.stats) dyn = ((size_t)(3 * a.max_steps) * 4 + 7) / 8 * 8 + (size_t)a.max_steps * 8;
   const dim3 grid(a.S * a.LH), block(kThreads);

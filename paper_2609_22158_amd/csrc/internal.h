@@ -47,8 +47,11 @@ struct FuseArgs {
   void* stats;               // stepkv_step_stat [L*Hkv][cu_steps[S]] or null
   uint32_t* status;          // device status word (STEPKV_FLAG_*) or null
   int S, LH, ntot, total_steps, half, max_steps, max_len;
+  int total_chunks;          // prio_chunks(): workgroups per row without statistics
   float alpha, beta;
 };
+// Chunks of 2048 positions over the sequences (the priority without statistics).
+int prio_chunks(const int32_t* cu_seqlens_host, int S);
 hipError_t launch_fuse(const FuseArgs& a, hipStream_t st);
 
 // Shared-index priority without step statistics, over chunks of 256 positions.

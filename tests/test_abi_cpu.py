@@ -16,6 +16,7 @@ from synth import make_workload
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "stepkv.h")
 FAKE = 0x10000  # placeholder device address; never dereferenced by these calls
+FAR = 1 << 44  # another placeholder, far enough from FAKE that no array here spans both
 
 
 @pytest.fixture(scope="module")
@@ -166,6 +167,13 @@ def test_saliency_priority_reject(lib):
                need, None) == B.EUNSUPPORTED
     pri = lib.stepkv_priority
     assert pri(ctypes.byref(pb), ctypes.byref(prm), None, FAKE, FAKE, FAKE, FAKE, None,
+               None) == B.EINVAL
+    # saliency and scores sharing memory (the row-spread priority keeps partial maxima in
+    # the scores rows while other workgroups still read the saliency around them)
+    n = 2 * 2 * 3000 * 4  # L * Hkv * Ntot floats
+    assert pri(ctypes.byref(pb), ctypes.byref(prm), FAKE, FAKE, FAKE, FAKE, FAKE, None,
+               None) == B.EINVAL
+    assert pri(ctypes.byref(pb), ctypes.byref(prm), FAKE + n - 4, FAKE, FAKE, FAKE, FAKE, None,
                None) == B.EINVAL
     assert pri(ctypes.byref(pb), ctypes.byref(B.Params(pool_kernel=0).c()), FAKE, FAKE, FAKE,
                FAKE, FAKE, None, None) == B.EINVAL
@@ -349,7 +357,7 @@ def test_score_noalloc_rejects(lib):
     prm = B.Params().c()
 
     def call(pb, p=prm, **kw):
-        a = dict(q=FAKE, k=FAKE, sid=FAKE, prot=FAKE, util=FAKE, scores=FAKE, sal=FAKE,
+        a = dict(q=FAKE, k=FAKE, sid=FAKE, prot=FAKE, util=FAKE, scores=FAKE, sal=FAR,
                  stats=None)
         a.update(kw)
         return lib.stepkv_score_noalloc(ctypes.byref(pb), ctypes.byref(p) if p else None,
@@ -358,6 +366,7 @@ def test_score_noalloc_rejects(lib):
 
     pb = _problem()
     assert call(pb, sal=None) == B.EINVAL  # the saliency buffer is required here
+    assert call(pb, sal=FAKE + 4) == B.EINVAL  # saliency overlapping the scores
     assert call(pb, p=None) == B.EINVAL
     assert call(pb, q=None) == B.EINVAL
     assert call(pb, scores=None) == B.EINVAL
