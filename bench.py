@@ -14,7 +14,10 @@ around each C ABI call, on the launch stream) and the saliency roofline come
 from a second pass of the same K steps. A third pass writes --flush-mib bytes
 before each step (evicting the Infinity Cache) and times every step from the
 cold cache with its own events ("flushed"); "hbm_ceilings" gives the read and
-copy bandwidth of plain streaming kernels with the compaction's access width.
+copy bandwidth of plain streaming kernels with the compaction's access width;
+"mfma_issue" gives the bf16 MFMA rate of a probe at the sweeps' occupancy, alone
+and with the sweeps' vector work per MFMA (an exp2, an FMA and an add for each
+of two score elements), and their ratio, the share of MFMA issue that mix leaves.
 
 By default the saliency is computed from the window queries and the cache
 alone (two sweeps over K). With --lse-fed the window rows' log-sum-exps are
@@ -77,6 +80,9 @@ def parse():
                          "256 MB Infinity Cache); 0 skips that pass")
     ap.add_argument("--ceiling-mib", type=int, default=1024,
                     help="buffer size of the HBM read and copy ceiling probes; 0 skips them")
+    ap.add_argument("--issue-probe-iters", type=int, default=4000,
+                    help="loops of the MFMA issue-rate probe (MFMAs alone, then with the "
+                         "saliency sweeps' vector work per MFMA); 0 skips it")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this size (HBM counter calibration)")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -513,6 +519,25 @@ def main():
         res["bytes"] = nb
         ceilings = res
         del src_buf, dst_buf
+    issue = None
+    if args.issue_probe_iters > 0:  # the MFMA rate the sweeps' instruction mix leaves
+        blocks = 512  # 2 workgroups of 4 waves per CU: the sweeps' 2 waves per SIMD
+        sink = torch.empty(blocks * 256, dtype=torch.float32, device=dev)
+        flops = blocks * 4 * args.issue_probe_iters * 4 * 32768.0
+        res = {}
+        for name, mix in (("mfma_only_tflops", False), ("with_sweep_mix_tflops", True)):
+            B.issue_probe(mix, blocks, args.issue_probe_iters, sink)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(5):
+                B.issue_probe(mix, blocks, args.issue_probe_iters, sink)
+            e1.record(stream)
+            e1.synchronize()
+            res[name] = round(flops / (e0.elapsed_time(e1) * 1e-3 / 5) / 1e12, 1)
+        res["mix_share"] = round(res["with_sweep_mix_tflops"] / res["mfma_only_tflops"], 4)
+        issue = res
+        del sink
 
     tokens = float(ntot)
     value = tokens / (ms_per_step * 1e-3)
@@ -590,6 +615,8 @@ def main():
         line["flushed"] = flushed
     if ceilings:
         line["hbm_ceilings"] = ceilings
+    if issue:
+        line["mfma_issue"] = issue
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = (cpu_baseline_shared(w, budget, args.cpu_seconds, params, n_sh)
                                 if shared else

@@ -486,6 +486,18 @@ int stepkv_decode_attention(const stepkv_problem* pb, const void* q_dec, const v
  * `stream`. Errors: EINVAL, EHIP. */
 int stepkv_bandwidth_probe(const void* src, void* dst, size_t bytes, int32_t copy, void* stream);
 
+/* Issue-rate probe (not part of the method): the share of the matrix cores'
+ * issue rate that the saliency sweeps' instruction mix leaves on this
+ * device. Each wave of `blocks` workgroups of 256 threads loops `iters` times
+ * over four independent v_mfma_f32_32x32x16_bf16 (32768 flops each); with
+ * mix = 1 every MFMA is followed by the sweeps' vector work for two score
+ * elements (a v_fma_f32, a v_exp_f32 and a v_add_f32 each, on independent
+ * chains). Timing the call with mix 0 and with mix 1 on the same grid gives
+ * the MFMA rate with and without that work. sink receives blocks * 256
+ * floats (device memory, caller-owned). Asynchronous on `stream`.
+ * Errors: EINVAL (mix not 0 or 1, blocks or iters below 1, null sink), EHIP. */
+int stepkv_issue_probe(int32_t mix, int32_t blocks, int32_t iters, float* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

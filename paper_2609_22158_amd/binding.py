@@ -105,6 +105,8 @@ _SIGNATURES = {
                                        _vp, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp,
                                        _vp, ctypes.c_int32, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     "stepkv_bandwidth_probe": (ctypes.c_int, [_vp, _vp, ctypes.c_size_t, ctypes.c_int32, _vp]),
+    "stepkv_issue_probe": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp,
+                                          _vp]),
     "stepkv_score_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
     "stepkv_saliency_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ProblemC)]),
     "stepkv_saliency": (ctypes.c_int, [ctypes.POINTER(ProblemC), ctypes.POINTER(ParamsC), _vp,
@@ -809,6 +811,16 @@ def bandwidth_probe(src, dst, copy: bool, stream=None) -> None:
         raise ValueError("dst too small")
     _check("stepkv_bandwidth_probe", load().stepkv_bandwidth_probe(
         src.data_ptr(), dst.data_ptr(), nbytes, int(bool(copy)), _stream(stream)))
+
+
+def issue_probe(mix: bool, blocks: int, iters: int, sink, stream=None) -> None:
+    """stepkv_issue_probe: four 32x32x16 bf16 MFMAs per loop per wave, alone (mix False) or
+    with the saliency sweeps' vector work for two score elements per MFMA; sink a float32
+    CUDA tensor of at least blocks * 256 elements."""
+    if sink.numel() < blocks * 256 or sink.dtype.itemsize != 4:
+        raise ValueError("sink too small")
+    _check("stepkv_issue_probe", load().stepkv_issue_probe(int(bool(mix)), int(blocks), int(iters),
+                                                           sink.data_ptr(), _stream(stream)))
 
 
 def bf16_from_bits(bits: np.ndarray, device="cuda"):

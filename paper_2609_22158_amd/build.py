@@ -19,7 +19,7 @@ C_DEMO_SRC = os.path.join(ROOT, "tests", "c_abi", "compress_demo.c")
 C_DEMO = os.path.join(ROOT, "tests", "c_abi", "compress_demo")
 
 SOURCES = ["api.cpp", "step_text.cpp", "saliency.hip", "fuse.hip", "select.hip", "compact.hip",
-           "decode.hip", "scratch.hip"]
+           "decode.hip", "scratch.hip", "probe.hip"]
 ARCH = "gfx950"
 
 

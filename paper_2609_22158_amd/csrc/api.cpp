@@ -721,6 +721,11 @@ int stepkv_bandwidth_probe(const void* src, void* dst, size_t bytes, int32_t cop
   return hip_status(launch_probe(src, dst, bytes, copy, static_cast<hipStream_t>(stream)));
 }
 
+int stepkv_issue_probe(int32_t mix, int32_t blocks, int32_t iters, float* sink, void* stream) {
+  if ((mix != 0 && mix != 1) || blocks < 1 || iters < 1 || !sink) return STEPKV_EINVAL;
+  return hip_status(launch_issue_probe(mix, blocks, iters, sink, static_cast<hipStream_t>(stream)));
+}
+
 size_t stepkv_decode_workspace_bytes(const stepkv_problem* pb, int32_t out_rows) {
   if (check_problem(pb) != STEPKV_OK || out_rows < 0) return 0;
   DecodeArgs a{};

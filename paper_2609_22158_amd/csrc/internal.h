@@ -144,4 +144,9 @@ int decode_total_splits(const int32_t* cu_seqlens_host, int S, int out_rows, int
 size_t decode_partial_floats(const DecodeArgs& a);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t st);
 
+// Issue-rate probe: `blocks` workgroups of 256 threads, `iters` loops of four
+// 32x32x16 bf16 MFMAs, alone (mix 0) or with the saliency sweeps' vector work
+// for two score elements per MFMA (mix 1); one float per thread to sink.
+hipError_t launch_issue_probe(int mix, int blocks, int iters, float* sink, hipStream_t st);
+
 }  // namespace stepkv

@@ -32,7 +32,7 @@ def _declared_functions():
 
 def test_exports_every_declared_function(lib):
     names = _declared_functions()
-    assert len(names) == 30, names
+    assert len(names) == 31, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B._SIGNATURES)
@@ -378,6 +378,15 @@ def test_score_noalloc_rejects(lib):
     assert lib.stepkv_saliency_workspace_bytes(ctypes.byref(big)) > B.STATIC_SCRATCH_BYTES
     assert call(big) == B.ESCRATCH
     assert "static scratch" in B.strerror(B.ESCRATCH)
+
+
+def test_issue_probe_rejects(lib):
+    f = lib.stepkv_issue_probe
+    assert f(2, 512, 10, FAKE, None) == B.EINVAL
+    assert f(-1, 512, 10, FAKE, None) == B.EINVAL
+    assert f(0, 0, 10, FAKE, None) == B.EINVAL
+    assert f(1, 512, 0, FAKE, None) == B.EINVAL
+    assert f(1, 512, 10, None, None) == B.EINVAL
 
 
 def test_bandwidth_probe_rejects(lib):
