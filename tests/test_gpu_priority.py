@@ -70,3 +70,40 @@ def test_row_spread_priority_matches_per_sequence_kernels_and_oracle(pool):
                 T = O.pooled_saliency(sal[l, h, a:b].astype(np.float64), prun, pool)
                 ref = O.priority(O.normalised_saliency(T, prun), sid[a:b], S, prun, 0.3, 0.7)
                 close(spread[l, h, a:b], ref, f"P{(s, l, h)} pool {pool}")
+
+
+def test_row_spread_priority_reports_conditions():
+    """The row-spread path's checked variant (a status word in the problem): the inputs above
+    hold prunable tokens with out-of-range step ids (STEPKV_FLAG_STEP_ID); a NaN saliency adds
+    STEPKV_FLAG_NONFINITE; with every step id in range and finite inputs nothing is reported.
+    The scores are the unchecked variant's in every case."""
+    import torch
+
+    from paper_2609_22158_amd import binding as B
+
+    cu, cu_steps, sal, prot, sid, util = _inputs(77)
+    L, Hkv = sal.shape[:2]
+    pb = B.Problem(L, 4 * Hkv, Hkv, 128, 32, cu, cu_steps, status=True)
+    quiet = B.Problem(L, 4 * Hkv, Hkv, 128, 32, cu, cu_steps, status=False)
+    prm = B.Params(pool_kernel=7)
+    clean_sid = sid.copy()
+    for s in range(len(SEQLENS)):
+        a, b = int(cu[s]), int(cu[s + 1])
+        n = int(cu_steps[s + 1] - cu_steps[s])
+        clean_sid[a:b] = np.clip(sid[a:b], 0, n - 1)
+    nan_sal = sal.copy()
+    nan_sal[3, 2, int(cu[7]) + 12345] = np.nan  # a prunable position of the 40000-token sequence
+    prot_n = prot.copy()
+    prot_n[int(cu[7]) + 12345] = 0
+    cases = [("bad step ids", sal, sid, prot, B.FLAG_STEP_ID),
+             ("clean", sal, clean_sid, prot, 0),
+             ("NaN saliency", nan_sal, clean_sid, prot_n, B.FLAG_NONFINITE),
+             ("both", nan_sal, sid, prot_n, B.FLAG_STEP_ID | B.FLAG_NONFINITE)]
+    pb.status(clear=True)
+    for what, a_, s_, p_, want in cases:
+        args = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in (a_, s_, p_, util)]
+        log(f"[priority flags] {what}")
+        checked = B.priority(pb, *args, prm)["scores"].cpu().numpy()
+        assert pb.status(clear=True) == want, what
+        plain = B.priority(quiet, *args, prm)["scores"].cpu().numpy()
+        assert np.array_equal(checked.view(np.uint32), plain.view(np.uint32)), what
