@@ -467,10 +467,15 @@ size_t stepkv_decode_workspace_bytes(const stepkv_problem* pb, int32_t out_rows)
  * out fp32 [L][S][Hq][d] (zero for a sequence with no row); scale <= 0
  * selects 1/sqrt(d); k_hat and v_hat may be NULL when out_rows is 0. Rows at
  * or past out_rows are not read (STEPKV_FLAG_OUT_ROWS in pb->status when
- * cu_retained[S] exceeds out_rows). Each KV head's rows are read once for its whole query
- * group, split over workgroups of 512 rows. Errors: EINVAL, EUNSUPPORTED
- * (d), EWORKSPACE (below stepkv_decode_workspace_bytes, or not 256-byte
- * aligned), EHIP. */
+ * cu_retained[S] exceeds out_rows; each sequence's range of cu_retained is
+ * clamped to [0, out_rows)). Each KV head's rows are read once for its whole
+ * query group (up to 16 heads; wider groups are served per query head),
+ * split over workgroups of 512 rows, or 1024 rows when
+ * L * Hkv * floor(out_rows / 1024) >= 1536. The workspace holds one partial
+ * state (d + 2 floats) per (layer, KV head, split, head of the group), for
+ * the splits min(sum_s ceil(min(N_s, out_rows) / split),
+ * floor(out_rows / split) + S). Errors: EINVAL, EUNSUPPORTED (d), EWORKSPACE
+ * (below stepkv_decode_workspace_bytes, or not 256-byte aligned), EHIP. */
 int stepkv_decode_attention(const stepkv_problem* pb, const void* q_dec, const void* k_hat,
                             const void* v_hat, const int32_t* cu_retained, int32_t out_rows,
                             float scale, float* out, void* workspace, size_t ws_bytes,
