@@ -98,8 +98,6 @@ __global__ __launch_bounds__(kThreads) void decode_simple_kernel(DecodeArgs a) {
   }
 }
 
-
-
 // Row splits of sequence s: ceil(R_s / split_rows).
 __device__ __forceinline__ int splits_of(const DecodeArgs& a, int s) {
   int r0;
@@ -141,17 +139,17 @@ typedef float f32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
 
 // One workgroup per (layer, KV head, sequence, split of split_rows retained
 // rows); each wave takes a quarter of the split in tiles of 16 rows, keeps its
-// own online-softmax state and its own ring of NST tiles in flight: K to
-// registers, V straight to LDS (global_load_lds), tile t + NST - 1 issued
-// before tile t is computed. Both products run on MFMA with the query group as
+// own online-softmax state and its own ring of kStages tiles: K to registers,
+// V straight to LDS (global_load_lds), tile t + kStages - 1 issued before
+// tile t is computed. Both products run on MFMA with the query group as
 // 16 columns (heads past G are zero):
 //  - S = K_tile Q^T on v_mfma_f32_16x16x32_bf16: A = the 16 key rows, B = the
 //    query heads. Lane group g = l / 16 reads 16-byte pieces 4 ks + g of its
 //    row for k-step ks (64 contiguous bytes per row and load; the query takes
 //    the same d order). Lane l then holds head l % 16 for rows 4 g + 0..3.
-//  - Softmax per head in that layout: a reference per head that moves only
-//    when a logit passes it by more than 2^kSlack (so p <= 2^kSlack and
-//    rescaling is rare), p = 2^(x - m).
+//  - Softmax per head in that layout, in the log2 domain: a reference m per
+//    head that moves only when a logit exceeds it by more than kSlack (so
+//    p = 2^(x - m) <= 2^kSlack and rescaling is rare).
 //  - O += P V on v_mfma_f32_16x16x16_bf16: A = P as the lanes hold it (head
 //    l % 16, rows 4 g + 0..3), split into bf16 hi + lo parts (P to about
 //    2^-17 relative); B = 16 value columns of those rows, read from the LDS
