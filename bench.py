@@ -91,8 +91,7 @@ def parse():
     return ap.parse_args()
 
 
-SALIENCY_KERNELS = ("saliency_kernel", "lse_combine_kernel", "lse_import_kernel",
-                    "chunk_plan_kernel")
+SALIENCY_KERNELS = ("saliency_kernel", "lse_combine_kernel", "lse_import_kernel")
 
 
 def _saliency_part(name: str, lse_fed: bool):
@@ -112,6 +111,7 @@ def _saliency_part(name: str, lse_fed: bool):
 def record_traffic(args) -> None:
     """HBM bytes per saliency launch, scaled by the counters' reading of a plain copy."""
     import csv
+    import re
     from collections import defaultdict
 
     def per_dispatch(path, counter):
@@ -134,13 +134,13 @@ def record_traffic(args) -> None:
         copies = [d for d in vals if "copyBuffer" in names[d]]
         cal = probe / (max(vals[d] for d in copies) * 1024.0)  # bytes per counted byte
         per_kernel = defaultdict(list)
-        plans = sorted((int(d) for d in vals if "chunk_plan_kernel" in names[d]))
+        launches = 0  # saliency stages: each runs the column-sum sweep exactly once
         for d, v in vals.items():
             k = _saliency_part(names[d], args.lse_fed)
-            if k is None or (args.lse_fed and k == "chunk_plan_kernel" and int(d) == plans[0]):
-                continue  # the first plan of an LSE-fed run belongs to the untimed row-LSE call
+            if k is None:
+                continue
             per_kernel[k].append(v * 1024.0 * cal)
-        launches = len(per_kernel["chunk_plan_kernel"])  # one per saliency launch
+            launches += bool(re.search(r"saliency_kernel<\d+, \d+, 2[,>]", names[d]))
         out[counter] = {"calibration": cal, "launches": launches,
                         "bytes": sum(sum(v) for v in per_kernel.values()) / launches,
                         "per_kernel": {k: sum(v) / launches for k, v in per_kernel.items()}}

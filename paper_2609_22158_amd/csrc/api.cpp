@@ -97,7 +97,7 @@ SaliencyPlan plan_saliency(const stepkv_problem* pb) {
 }
 
 struct WsLayout {
-  size_t cu_chunks, partial, lse, sal, total;
+  size_t partial, lse, sal, total;
 };
 
 WsLayout layout(const stepkv_problem* pb, const SaliencyPlan& p) {
@@ -105,8 +105,6 @@ WsLayout layout(const stepkv_problem* pb, const SaliencyPlan& p) {
   const size_t ntot = (size_t)pb->cu_seqlens_host[pb->num_seqs];
   WsLayout w;
   size_t off = 0;
-  w.cu_chunks = off;
-  off = align_up(off + sizeof(int32_t) * (pb->num_seqs + 1));
   w.partial = off;
   off = align_up(off + sizeof(float) * 2 * lh * p.total_chunks * p.rows_pad);
   w.lse = off;
@@ -266,7 +264,6 @@ int run_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void*
   sa.q = static_cast<const uint16_t*>(q_win);
   sa.k = static_cast<const uint16_t*>(k);
   sa.cu_seqlens = pb->cu_seqlens;
-  sa.cu_chunks = reinterpret_cast<int32_t*>(ws + w.cu_chunks);
   sa.partial = reinterpret_cast<float2*>(ws + w.partial);
   sa.lse2 = reinterpret_cast<float*>(ws + w.lse);
   sa.sal = sal;

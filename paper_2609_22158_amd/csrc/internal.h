@@ -14,7 +14,6 @@ struct SaliencyArgs {
   const uint16_t* q;         // bf16 [L][S][W][Hq][d]
   const uint16_t* k;         // bf16 [L*Hkv][Ntot][d]
   const int32_t* cu_seqlens; // [S+1]
-  int32_t* cu_chunks;        // [S+1] chunk prefix (written by the plan kernel)
   float2* partial;           // [L*Hkv][total_chunks][rows_pad] (log2 max, sum)
   float* lse2;               // [S][L*Hkv][rows_pad] log2-domain log-sum-exp
   float* sal;                // [L*Hkv][Ntot] A_i

@@ -90,17 +90,51 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-__global__ void chunk_plan_kernel(const int32_t* __restrict__ cu_seqlens,
-                                  int32_t* __restrict__ cu_chunks, int S, int chunk) {
-  if (threadIdx.x == 0) {
-    int acc = 0;
-    cu_chunks[0] = 0;
-    for (int s = 0; s < S; ++s) {
-      const int n = cu_seqlens[s + 1] - cu_seqlens[s];
-      acc += (n + chunk - 1) / chunk;
-      cu_chunks[s + 1] = acc;
+// Key chunks of sequence s: ceil(N_s / chunk).
+__device__ __forceinline__ int chunks_of(const SaliencyArgs& a, int s) {
+  return (a.cu_seqlens[s + 1] - a.cu_seqlens[s] + a.chunk - 1) / a.chunk;
+}
+
+// The sequence s holding global chunk g (chunks of the sequences in order) and
+// its first global chunk: a wave-wide prefix over 64 sequences at a time, in
+// every wave (g is below the chunk total, so some sequence holds it).
+__device__ __forceinline__ void locate_chunk(const SaliencyArgs& a, int g, int& s_out,
+                                             int& first_out) {
+  const int lane = threadIdx.x & 63;
+  int base = 0;
+  s_out = a.S - 1;
+  first_out = 0;
+  for (int s0 = 0; s0 < a.S; s0 += kWave) {
+    const int sq = s0 + lane;
+    const int cnt = sq < a.S ? chunks_of(a, sq) : 0;
+    int incl = cnt;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int o = __shfl_up(incl, off, kWave);
+      if (lane >= off) incl += o;
     }
+    const int total = __shfl(incl, kWave - 1, kWave);
+    if (g < base + total) {
+      const int first = __builtin_ctzll(ballot(base + incl > g));
+      s_out = s0 + first;
+      first_out = base + __shfl(incl - cnt, first, kWave);
+      return;
+    }
+    base += total;
   }
+}
+
+// The first global chunk of sequence s: the chunks of the sequences before it.
+__device__ __forceinline__ int first_chunk(const SaliencyArgs& a, int s) {
+  const int lane = threadIdx.x & 63;
+  int acc = 0;
+  for (int s0 = 0; s0 < s; s0 += kWave) {
+    int cnt = s0 + lane < s ? chunks_of(a, s0 + lane) : 0;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
+    acc += cnt;
+  }
+  return acc;
 }
 
 // Calls f(std::integral_constant<int, I>{}) for I = B .. E-1, unrolled.
@@ -150,8 +184,10 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   int lh = blockIdx.x / a.total_chunks;
   const int rem_blk = blockIdx.x - lh * a.total_chunks;
   if (PASS == 2) lh = LH - 1 - lh;  // pass 2 starts where pass 1 ended (cache reuse)
-  const int s = segment_of(a.cu_chunks, a.S, rem_blk);
-  const int c = rem_blk - a.cu_chunks[s];
+  int s, cfirst;
+  locate_chunk(a, rem_blk, s, cfirst);
+  s = uniform(s);
+  const int c = uniform(rem_blk - cfirst);
   const int l = lh / a.Hkv, h = lh - l * a.Hkv;
   const int seq0 = a.cu_seqlens[s];
   const int ns = a.cu_seqlens[s + 1] - seq0;
@@ -627,7 +663,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     }
   }
   if (kg == 0 && hf == 0) {
-    float2* out = a.partial + ((size_t)lh * a.total_chunks + a.cu_chunks[s] + c) * a.rows_pad;
+    float2* out = a.partial + ((size_t)lh * a.total_chunks + rem_blk) * a.rows_pad;
 #pragma unroll
     for (int b = 0; b < 2; ++b) out[rg * 64 + b * 32 + col] = make_float2(m2[b], zs[b]);
   }
@@ -649,7 +685,7 @@ __global__ __launch_bounds__(kCombineThreads) void lse_combine_kernel(SaliencyAr
   const int s = blockIdx.x / LH, lh = blockIdx.x - s * LH;
   const int row = threadIdx.x % a.rows_pad, grp = threadIdx.x / a.rows_pad;
   const int ngrp = kCombineThreads / a.rows_pad;
-  const int c0 = a.cu_chunks[s], c1 = a.cu_chunks[s + 1];
+  const int c0 = first_chunk(a, s), c1 = c0 + chunks_of(a, s);
   const float2* __restrict__ pp = a.partial + (size_t)lh * a.total_chunks * a.rows_pad + row;
   // one online pass over this thread's chunks, eight loads in flight at a time;
   // a chunk whose keys this row never saw is (-inf, 0) and adds nothing
@@ -736,10 +772,6 @@ int saliency_rows_pad(int R) { return R <= 64 ? 64 : (R <= 128 ? 128 : 256); }
 int saliency_tile_keys(int R) { return 32 * (4 / (saliency_rows_pad(R) / 64)); }
 
 hipError_t launch_saliency(const SaliencyArgs& a, int d, SaliencyMode mode, hipStream_t st) {
-  hipLaunchKernelGGL(chunk_plan_kernel, dim3(1), dim3(64), 0, st, a.cu_seqlens, a.cu_chunks, a.S,
-                     a.chunk);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
   if (a.total_chunks == 0) {  // no keys at all: every exported row LSE is -inf
     if (mode == SaliencyMode::kLseOnly)
       hipLaunchKernelGGL(lse_combine_kernel, dim3(a.S * a.L * a.Hkv), dim3(kCombineThreads), 0, st,
