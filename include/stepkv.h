@@ -299,8 +299,9 @@ int stepkv_saliency_from_lse(const stepkv_problem* pb, const stepkv_params* prm,
  *   P_i  = alpha * Th_i + beta * S_{step_ids[i]};  protected: -inf
  * plus the optional per-step statistics (see stepkv_score). No workspace:
  * without statistics, and with more (sequence, layer, KV head) rows than
- * 256, each row is spread over workgroups of 2048 positions, which keep
- * their partial maxima in the scores row until they overwrite it.
+ * 256 or more than 4096 steps in a sequence, each row is spread over
+ * workgroups of 2048 positions, which keep their partial maxima in the
+ * scores row until they overwrite it.
  * Errors: EINVAL (also scores overlapping saliency), EUNSUPPORTED (pool
  * window, stats step count), EHIP. */
 int stepkv_priority(const stepkv_problem* pb, const stepkv_params* prm, const float* saliency,

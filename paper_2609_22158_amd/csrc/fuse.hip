@@ -708,7 +708,9 @@ hipError_t launch_fuse(const FuseArgs& a, hipStream_t st) {
   // kPrChunk positions. Measured on MI355X: 28 layers x 4 heads x 16 ragged
   // sequences 152 -> 118 us; with one round (32 x 8 rows of one 32k sequence)
   // the per-sequence kernel stays ahead, 37 against 41 us.
-  if (!a.stats && a.S * a.LH > 256) {
+  // Sequences with more than 4096 steps take the spread path too: the
+  // per-sequence kernels stage every step utility in LDS.
+  if (!a.stats && (a.S * a.LH > 256 || a.max_steps > 4096)) {
     if (a.total_chunks == 0) return hipSuccess;
     const dim3 grid((unsigned)a.LH * (unsigned)a.total_chunks);
     auto go = [&](auto half_c) {
