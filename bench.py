@@ -577,6 +577,9 @@ def main():
            "compact_gbps": round(compact_bytes / t_cmp / 1e9, 1),
            "compact_frac": round(compact_bytes / t_cmp / 1e9 / HBM_PEAK_GBS, 4),
            "peak_gbps": HBM_PEAK_GBS}
+    if traffic:  # the counted bytes of the saliency stage over its time
+        hbm.update({"saliency_measured_gbps": round(traffic / t_sal / 1e9, 1),
+                    "saliency_measured_frac": round(traffic / t_sal / 1e9 / HBM_PEAK_GBS, 4)})
     if args.decode:  # K_hat and V_hat read once (plus queries and outputs)
         dec_bytes = lh * out_rows * d * 2 * 2 + q_dec.numel() * 2 + dec_out.numel() * 4
         t_dec = stage_ms["decode"] * 1e-3
