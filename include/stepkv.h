@@ -81,7 +81,7 @@ extern "C" {
 #define STEPKV_ESCRATCH (-5)     /* the problem needs more than the static scratch */
 
 /* Limits of this build (STEPKV_EUNSUPPORTED beyond them). */
-#define STEPKV_MAX_WINDOW_ROWS 256   /* W * G */
+#define STEPKV_MAX_WINDOW_ROWS 2048  /* W * G (above 256: one pair of sweeps per 256 rows) */
 #define STEPKV_MAX_POOL_KERNEL 63    /* odd pooling window */
 #define STEPKV_MAX_STEPS_STATS 4096  /* steps per sequence when stats are requested */
 #define STEPKV_CUE_CAP 64            /* evidence cues per text field (App. D) */
@@ -261,7 +261,9 @@ size_t stepkv_saliency_workspace_bytes(const stepkv_problem* pb);
  * fp32 [L][Hkv][Ntot]. Window rows r = w*G + g use query head h*G + g; the
  * softmax runs over the keys each row sees (all N_s keys, or the causal tail
  * of prm->causal_tail). Computed exactly (two sweeps over K: row
- * log-sum-exp, then column sums), fp32 accumulation of bf16 products.
+ * log-sum-exp, then column sums), fp32 accumulation of bf16 products. Window
+ * rows (r = w * G + g) run in groups of 256, one pair of sweeps per group; the
+ * column sums of a later group are added to the earlier groups' in order.
  * Errors: EINVAL (null pointers, bad problem or scale), EUNSUPPORTED (d not in
  * {64,128} or W*G > STEPKV_MAX_WINDOW_ROWS), EWORKSPACE, EHIP. */
 int stepkv_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,

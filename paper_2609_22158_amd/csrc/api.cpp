@@ -64,10 +64,13 @@ struct SaliencyPlan {
   int R, rows_pad, chunk, total_chunks;
 };
 
+// Window rows per pair of sweeps (the MFMA tiling holds at most 256).
+constexpr int kRowGroup = 256;
+
 SaliencyPlan plan_saliency(const stepkv_problem* pb) {
   SaliencyPlan p;
   p.R = window_rows(pb);
-  p.rows_pad = saliency_rows_pad(p.R);
+  p.rows_pad = saliency_rows_pad(std::min(p.R, kRowGroup));  // the first (widest) group
   const int64_t lh = (int64_t)pb->num_layers * pb->num_kv_heads;
   auto chunks_for = [&](int c) {
     int64_t t = 0;
@@ -81,7 +84,7 @@ SaliencyPlan plan_saliency(const stepkv_problem* pb) {
   // stop at 4096 keys: with several rounds the two workgroups of a compute
   // unit drift apart and each one's start hides under the other's sweep,
   // which a single round of simultaneous starts does not allow.
-  const int tile = saliency_tile_keys(p.R);
+  const int tile = saliency_tile_keys(std::min(p.R, kRowGroup));
   p.chunk = 128;
   int64_t best = -1;
   for (int c = 128; c <= 4096; c += 128) {
@@ -276,14 +279,23 @@ int run_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void*
   sa.Hq = pb->num_q_heads;
   sa.Hkv = pb->num_kv_heads;
   sa.G = pb->num_q_heads / pb->num_kv_heads;
-  sa.R = plan.R;
-  sa.rows_pad = plan.rows_pad;
   sa.ntot = pb->cu_seqlens_host[pb->num_seqs];
   sa.chunk = plan.chunk;
   sa.total_chunks = plan.total_chunks;
   const double scale = prm->scale > 0.0f ? (double)prm->scale : 1.0 / std::sqrt((double)d);
   sa.c = (float)(scale * 1.4426950408889634);  // log2(e)
-  return hip_status(launch_saliency(sa, d, mode, st));
+  // Window rows in groups of at most 256, one pair of sweeps per group: a
+  // row's LSE needs only its own logits, and the column sums of the later
+  // groups add to the first group's (the workspace regions are reused).
+  for (int row0 = 0; row0 < plan.R; row0 += kRowGroup) {
+    sa.row0 = row0;
+    sa.R = std::min(kRowGroup, plan.R - row0);
+    sa.rows_pad = saliency_rows_pad(sa.R);
+    sa.accumulate = row0 > 0;
+    const int rc = hip_status(launch_saliency(sa, d, mode, st));
+    if (rc != STEPKV_OK) return rc;
+  }
+  return STEPKV_OK;
 }
 
 int run_priority(const stepkv_problem* pb, const stepkv_params* prm, const float* sal,

@@ -19,7 +19,11 @@ struct SaliencyArgs {
   float* sal;                // [L*Hkv][Ntot] A_i
   const float* lse_in;       // [L][S][W][Hq] natural-log row LSE given by the caller
   float* lse_out;            // [L][S][W][Hq] natural-log row LSE exported (or null)
-  int L, S, W, Hq, Hkv, G, R, rows_pad;
+  int L, S, W, Hq, Hkv, G;
+  int row0;      // first window row (w * G + g) of this launch's row group
+  int R;         // window rows in the group (at most 256)
+  int rows_pad;  // R padded to 64, 128 or 256
+  int accumulate;  // nonzero: the column-sum sweep adds to sal (groups after the first)
   int ntot, chunk, total_chunks;
   int causal;  // nonzero: window slot w sees keys 0 .. N_s - W + w only
   float c;     // softmax scale * log2(e)

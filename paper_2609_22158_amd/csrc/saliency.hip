@@ -196,13 +196,14 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   const int ntiles = (nkeys + TILE - 1) / TILE;
   const uint16_t* __restrict__ kseq = a.k + ((size_t)lh * a.ntot + seq0) * D;
 
-  // ---- window rows of this wave: two 32-row blocks, k-slices (D/2)*hf + 8*st
+  // ---- window rows of this wave: two 32-row blocks of the launch's row group
+  // (rows row0 + local row), k-slices (D/2)*hf + 8*st
   bf16x8_t qf[2][KSTEPS];
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
     const int row = rg * 64 + b * 32 + col;
     if (row < a.R) {
-      const int w = row / a.G, g = row - w * a.G;
+      const int w = (a.row0 + row) / a.G, g = (a.row0 + row) - w * a.G;
       const uint16_t* qp =
           a.q + ((((size_t)l * a.S + s) * a.W + w) * a.Hq + h * a.G + g) * D + (D / 2) * hf;
 #pragma unroll
@@ -302,7 +303,10 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
         sum += rp[w2 * 64 + 32 + col2];
       }
       const int key = t * TILE + tid;
-      if (key < nkeys) a.sal[(size_t)lh * a.ntot + seq0 + key0 + key] = sum;
+      if (key < nkeys) {
+        float* o = a.sal + (size_t)lh * a.ntot + seq0 + key0 + key;
+        *o = a.accumulate ? *o + sum : sum;
+      }
     }
   };
 
@@ -314,19 +318,20 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     return CAUSAL && key0 + (t + 1) * TILE > hidden_from;
   };
   auto mask_hidden = [&](f32x16_t(&acc)[2], int t) __attribute__((always_inline)) {
-    // key kin of the tile is visible to window row `row` iff kin <= lim + row / G
+    // key kin of the tile is visible to window row `row` (row0 + the local row)
+    // iff kin <= lim + row / G
     const int lim = ns - a.W - key0 - t * TILE;
     if (PASS == 1) {  // lane: one row per block; keys kg*32 + 4*hf + 8*(j/4) + (j%4)
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
-        const int thr = lim + (rg * 64 + b * 32 + col) / a.G - kg * 32 - 4 * hf;
+        const int thr = lim + (a.row0 + rg * 64 + b * 32 + col) / a.G - kg * 32 - 4 * hf;
 #pragma unroll
         for (int j = 0; j < 16; ++j)
           if (8 * (j >> 2) + (j & 3) > thr) acc[b][j] = -INFINITY;
       }
     } else {  // lane: key kg*32 + col; rows rg*64 + 4*hf + 32*b + 8*(j/4) + (j%4)
       // row / G >= kin - lim  <=>  row >= G * (kin - lim)
-      const int thr = a.G * (kg * 32 + col - lim) - rg * 64 - 4 * hf;
+      const int thr = a.G * (kg * 32 + col - lim) - a.row0 - rg * 64 - 4 * hf;
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -554,7 +559,8 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
         float sum = part[0];
 #pragma unroll
         for (int k2 = 1; k2 < 2 * RG; ++k2) sum += part[k2];
-        a.sal[(size_t)lh * a.ntot + seq0 + key0 + rt * TILE + rtid] = sum;
+        float* o = a.sal + (size_t)lh * a.ntot + seq0 + key0 + rt * TILE + rtid;
+        *o = a.accumulate ? *o + sum : sum;
       }
     }
   };
@@ -722,7 +728,7 @@ __global__ __launch_bounds__(kCombineThreads) void lse_combine_kernel(SaliencyAr
   a.lse2[((size_t)s * LH + lh) * a.rows_pad + row] = l2;
   if (a.lse_out && row < a.R) {
     const int l = lh / a.Hkv, h = lh - l * a.Hkv;
-    const int w = row / a.G, g = row - w * a.G;
+    const int w = (a.row0 + row) / a.G, g = (a.row0 + row) - w * a.G;
     a.lse_out[(((size_t)l * a.S + s) * a.W + w) * a.Hq + h * a.G + g] =
         seen ? l2 * 0.693147180559945309f : -INFINITY;
   }
@@ -738,7 +744,7 @@ __global__ void lse_import_kernel(SaliencyArgs a) {
   float l2 = INFINITY;
   if (row < a.R) {
     const int l = lh / a.Hkv, h = lh - l * a.Hkv;
-    const int w = row / a.G, g = row - w * a.G;
+    const int w = (a.row0 + row) / a.G, g = (a.row0 + row) - w * a.G;
     const float x = a.lse_in[(((size_t)l * a.S + s) * a.W + w) * a.Hq + h * a.G + g];
     if (x != -INFINITY) l2 = x * 1.44269504088896341f;
   }

@@ -129,7 +129,7 @@ def test_workspace_bytes(lib):
     (dict(Hq=7), B.EINVAL),          # G not an integer
     (dict(d=96), B.EUNSUPPORTED),    # head dim
     (dict(d=0), B.EINVAL),
-    (dict(W=65, Hq=8, Hkv=2), B.EUNSUPPORTED),  # W*G = 260 > 256
+    (dict(W=513, Hq=8, Hkv=2), B.EUNSUPPORTED),  # W*G = 2052 > 2048
     (dict(cu=(0, 10, 5)), B.EINVAL),  # not monotone
     (dict(cu=(1, 10, 20)), B.EINVAL),  # does not start at 0
     (dict(L=0), B.EINVAL),
@@ -163,7 +163,7 @@ def test_saliency_priority_reject(lib):
                None) == B.EINVAL
     assert sal(ctypes.byref(pb), ctypes.byref(prm), FAKE, FAKE, FAKE, FAKE * 16, need - 256,
                None) == B.EWORKSPACE
-    assert sal(ctypes.byref(_problem(W=128)), ctypes.byref(prm), FAKE, FAKE, FAKE, FAKE * 16,
+    assert sal(ctypes.byref(_problem(W=513)), ctypes.byref(prm), FAKE, FAKE, FAKE, FAKE * 16,
                need, None) == B.EUNSUPPORTED
     pri = lib.stepkv_priority
     assert pri(ctypes.byref(pb), ctypes.byref(prm), None, FAKE, FAKE, FAKE, FAKE, None,
@@ -236,7 +236,7 @@ def test_lse_entry_points_reject(lib):
     assert lib.stepkv_score_from_lse(P, R, *args, full - 256, None) == B.EWORKSPACE
     args[2] = None  # lse
     assert lib.stepkv_score_from_lse(P, R, *args, full, None) == B.EINVAL
-    bad = _problem(W=65)
+    bad = _problem(W=513)
     assert lib.stepkv_saliency_from_lse(ctypes.byref(bad), R, FAKE, FAKE, FAKE, FAKE, FAKE * 16,
                                         need, None) == B.EUNSUPPORTED
 
@@ -339,7 +339,7 @@ def test_compress_workspace_and_rejects(lib):
     assert _compress(lib, pb, ws_bytes=need - 256) == B.EWORKSPACE
     assert _compress(lib, pb, ws=FAKE * 16 + 4) == B.EWORKSPACE
     assert _compress(lib, _problem(d=96)) == B.EUNSUPPORTED
-    assert _compress(lib, _problem(W=65)) == B.EUNSUPPORTED
+    assert _compress(lib, _problem(W=513)) == B.EUNSUPPORTED
 
 
 def test_status_read_rejects(lib):

@@ -23,6 +23,10 @@ CASES = {
     # W = 64 (W * G = 256 rows): the tail spans two 32-key tiles
     "l32_w64": dict(name="l32_32k", num_layers=1, seqlens=[3333, 64, 40], num_steps=12,
                     protected_len=16),
+    # W = 80 at G = 7: 560 window rows in three groups (256, 256, 48 rows; the last
+    # group on the 64-row tiling), each group's tail masked against its own rows
+    "ragged_w80": dict(name="ragged16", num_layers=1, window=80, seqlens=[2000, 70, 1, 900],
+                       protected_len=32),
 }
 
 _w = {}

@@ -15,7 +15,8 @@ from tests.gpu_cases import (HipRun, close, log, oracle_params, reduced, ref_row
 pytestmark = pytest.mark.gpu
 
 # sizes the oracle finishes in seconds, each spanning several key tiles and a
-# ragged tail, covering every window-row shape: W*G = 64, 128, 256, 224
+# ragged tail, covering every window-row shape: W*G = 64, 128, 256, 224, and 448
+# (two groups of window rows)
 CASES = {
     "tiny": dict(name="tiny"),  # the 1-layer, N=1024, d=64 configuration, unchanged
     "l1_8k": dict(name="l1_8k"),  # the 8B-shaped single layer, N=8192, unchanged
@@ -23,6 +24,9 @@ CASES = {
     "l32_32k_2l": dict(name="l32_32k", num_layers=2, seqlens=[5003], num_steps=20),
     "ragged_g7": dict(name="ragged16", num_layers=2, seqlens=[2500, 700, 130, 1, 0, 4097],
                       protected_len=64),
+    # W = 64 at G = 7: 448 window rows, two pairs of sweeps (256 and 192 rows)
+    "ragged_w64": dict(name="ragged16", num_layers=2, window=64, seqlens=[1500, 333, 0, 2100],
+                       protected_len=64),
 }
 
 _cache = {}

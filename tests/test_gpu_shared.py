@@ -20,6 +20,9 @@ CASES = {
     "ragged_g7": dict(name="ragged16", num_layers=2, seqlens=[2500, 700, 130, 1, 0, 4097],
                       protected_len=64),  # fewer layers than asked for: all of them
     "tiny": dict(name="tiny"),
+    # W = 48 at G = 7: 336 window rows per head, two pairs of sweeps
+    "ragged_w48": dict(name="ragged16", num_layers=3, window=48, seqlens=[1200, 90, 2222],
+                       protected_len=40),
 }
 LAST = 3
 
