@@ -1,7 +1,8 @@
 // Pooling, normalisation and step-utility fusion (Sec. 5.2, eq. token-priority).
-// Without step statistics and with more (sequence, head) rows than CUs, each
-// row is spread over workgroups of 2048 positions (prio_chunk_*). Otherwise
-// one workgroup per (sequence, head):
+// Without step statistics, and with more (sequence, head) rows than CUs or
+// more than 4096 steps in a sequence, each row is spread over workgroups of
+// 2048 positions (prio_chunk_*). Otherwise one workgroup per (sequence,
+// head). Both compute
 //   U_i  = sum_{|j-i| <= half} A_j [j prunable]     (k * T_i; zero padded)
 //   Th_i = U_i / max_{prunable} U                   (the 1/k cancels)
 //   P_i  = alpha * Th_i + beta * S[step_ids[i]]     (prunable; -inf if protected)
