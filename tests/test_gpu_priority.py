@@ -111,8 +111,9 @@ def test_row_spread_priority_reports_conditions():
 
 def test_many_steps_take_the_spread_path_against_oracle():
     """More than 4096 steps in a sequence (here 5000 steps of 2-3 tokens): the per-sequence
-    kernels would stage every step utility in LDS, so the row-spread path runs even for two
-    rows, reading the utilities from memory. Against the oracle's eq. token-priority."""
+    kernels would stage every step utility in LDS, so the row-spread path runs even for three
+    rows (a row count that leaves the last group of rows per workgroup partly empty), reading
+    the utilities from memory. Against the oracle's eq. token-priority."""
     import torch
 
     from paper_2609_22158_amd import binding as B
@@ -121,18 +122,18 @@ def test_many_steps_take_the_spread_path_against_oracle():
     n, nsteps = 12345, 5000
     cu = np.array([0, n], np.int32)
     cu_steps = np.array([0, nsteps], np.int32)
-    sal = rng.exponential(1.0, (1, 2, n)).astype(np.float32)
+    sal = rng.exponential(1.0, (1, 3, n)).astype(np.float32)
     prot = np.zeros(n, np.uint8)
     prot[:100] = 1
     sid = np.minimum(np.arange(n) * nsteps // n, nsteps - 1).astype(np.int32)
     util = rng.random(nsteps).astype(np.float32)
-    pb = B.Problem(1, 8, 2, 128, 32, cu, cu_steps, status=False)
+    pb = B.Problem(1, 12, 3, 128, 32, cu, cu_steps, status=False)
     prm = B.Params(alpha=0.4, beta=0.6, pool_kernel=7)
     log("[priority] 5000 steps in one sequence")
     got = B.priority(pb, *[torch.from_numpy(x).cuda() for x in (sal, sid, prot, util)],
                      prm)["scores"].cpu().numpy()
     prun = prot == 0
-    for h in range(2):
+    for h in range(3):
         T = O.pooled_saliency(sal[0, h].astype(np.float64), prun, 7)
         ref = O.priority(O.normalised_saliency(T, prun), sid, util.astype(np.float64), prun, 0.4, 0.6)
         close(got[0, h], ref, f"P head {h}")
