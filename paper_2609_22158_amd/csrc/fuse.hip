@@ -542,39 +542,68 @@ __device__ __forceinline__ void locate_chunk(const int32_t* __restrict__ cu_seql
 
 // (layer, KV head) rows per workgroup of the spread path: the rows share the
 // chunk's lookup, protected flags and step ids, and both rows' loads are in
-// flight at once (ragged batch: 118 -> 108 us; 4 rows, with half the
-// workgroups resident, 119 us).
+// flight at once (4 rows, with half the workgroups resident, measured slower).
 constexpr int kPrRows = 2;
 
-// am[i][e] = A of row lh0 + i at position p0 - half + e of the sequence when
-// that position exists and is prunable, else 0; e < kPrChunk + 2 half. Rows
-// past LH stage zeros. Every load of the chunk is issued before the first LDS
-// write.
-template <int NR>
-__device__ __forceinline__ void prio_stage(const FuseArgs& a, int lh0, int seq0, int ns, int p0,
-                                           float (*am)[kPrChunk + 2 * kMaxHalf]) {
+// The chunk's stage in LDS: am[i][e] = A of row lh0 + i at position
+// p0 - half + e of the sequence when that position exists and is prunable,
+// else 0, and pf[e] = 1 for such a prunable position; e < kPrChunk + 2 half.
+// Rows past LH stage zeros. Every load is issued before the first LDS write.
+// A chunk whose halos lie inside the sequence (all but the first and last of
+// a sequence) takes a path without clamps or range tests: the kernels are
+// bound by vector instructions, most of them address arithmetic.
+struct PrioStage {
+  float am[kPrRows][kPrChunk + 2 * kMaxHalf];
+  uint8_t pf[kPrChunk + 2 * kMaxHalf];
+};
+
+__device__ __forceinline__ void prio_stage(const FuseArgs& a, const float* const (&rowp)[kPrRows],
+                                           const uint8_t* __restrict__ prot, int ns, int p0,
+                                           PrioStage& st) {
   constexpr int J = kPrChunk / kPrThreads;
   const int tid = threadIdx.x;
-  const uint8_t* __restrict__ prot = a.prot + seq0;
-  float v[NR][J + 1];
+  const int q0 = p0 - a.half;  // position of stage entry 0
+  const int n_st = kPrChunk + 2 * a.half;
+  float v[kPrRows][J + 1];
   uint32_t pr[J + 1];
+  if (q0 >= 0 && q0 + n_st <= ns) {  // interior chunk (uniform)
 #pragma unroll
-  for (int j = 0; j <= J; ++j) {  // slot J: the 2 half halo positions past the chunk
-    const int e = tid + kPrThreads * j;
-    const int p = min(max(p0 - a.half + e, 0), max(ns - 1, 0));
-    pr[j] = prot[p];
+    for (int j = 0; j <= J; ++j) {
+      const int e = tid + kPrThreads * j;
+      const int q = q0 + min(e, n_st - 1);  // slot J: only the halo past the chunk is staged
+      pr[j] = prot[q];
 #pragma unroll
-    for (int i = 0; i < NR; ++i)
-      v[i][j] = lh0 + i < a.LH ? a.sal[(size_t)(lh0 + i) * a.ntot + seq0 + p] : 0.f;
-  }
+      for (int i = 0; i < kPrRows; ++i) v[i][j] = rowp[i][q];
+    }
 #pragma unroll
-  for (int j = 0; j <= J; ++j) {
-    const int e = tid + kPrThreads * j;
-    const int p = p0 - a.half + e;
-    const bool in = p >= 0 && p < ns && pr[j] == 0;
-    if (j < J || e < kPrChunk + 2 * a.half) {
+    for (int j = 0; j <= J; ++j) {
+      const int e = tid + kPrThreads * j;
+      if (j < J || e < n_st) {
+        const bool in = pr[j] == 0;
+        st.pf[e] = in;
 #pragma unroll
-      for (int i = 0; i < NR; ++i) am[i][e] = in ? v[i][j] : 0.f;
+        for (int i = 0; i < kPrRows; ++i) st.am[i][e] = in ? v[i][j] : 0.f;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j <= J; ++j) {
+      const int e = tid + kPrThreads * j;
+      const int q = min(max(q0 + e, 0), max(ns - 1, 0));
+      pr[j] = prot[q];
+#pragma unroll
+      for (int i = 0; i < kPrRows; ++i) v[i][j] = rowp[i][q];
+    }
+#pragma unroll
+    for (int j = 0; j <= J; ++j) {
+      const int e = tid + kPrThreads * j;
+      if (j < J || e < n_st) {
+        const int q = q0 + e;
+        const bool in = q >= 0 && q < ns && pr[j] == 0;
+        st.pf[e] = in;
+#pragma unroll
+        for (int i = 0; i < kPrRows; ++i) st.am[i][e] = in ? v[i][j] : 0.f;
+      }
     }
   }
 }
@@ -593,42 +622,57 @@ __device__ __forceinline__ float prio_pool(const float* am, int e, int half) {
   return acc;
 }
 
-template <int HALF>
-__global__ __launch_bounds__(kPrThreads) void prio_chunk_max_kernel(FuseArgs a) {
-  __shared__ float am[kPrRows][kPrChunk + 2 * kMaxHalf];
-  __shared__ float wred[kPrRows][kPrThreads / kWave];
+// The workgroup's rows and chunk: row group blockIdx / total_chunks (rows
+// lh0 .. lh0 + kPrRows - 1, pointers clamped to a real row past LH, whose
+// values the kernels never store), chunk g of the concatenated sequences.
+struct PrioWork {
+  int lh0, s, seq0, ns, p0;
+};
+
+__device__ __forceinline__ bool prio_work(const FuseArgs& a, PrioWork& w) {
   const int rgrp = blockIdx.x / a.total_chunks, g = blockIdx.x - rgrp * a.total_chunks;
-  const int lh0 = rgrp * kPrRows;
   int s, c;
   locate_chunk(a.cu_seqlens, a.S, g, s, c);
   s = uniform(s);
-  if (s < 0) return;
-  const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
-  const int p0 = uniform(c) * kPrChunk;
-  const uint8_t* prot = a.prot + seq0;
-  constexpr int J = kPrChunk / kPrThreads;
-  uint32_t pf[J];  // protected flags of this thread's positions
+  if (s < 0) return false;
+  w.lh0 = rgrp * kPrRows;
+  w.s = s;
+  w.seq0 = uniform(a.cu_seqlens[s]);
+  w.ns = uniform(a.cu_seqlens[s + 1]) - w.seq0;
+  w.p0 = uniform(c) * kPrChunk;
+  return true;
+}
+
+template <int HALF>
+__global__ __launch_bounds__(kPrThreads) void prio_chunk_max_kernel(FuseArgs a) {
+  __shared__ PrioStage st;
+  __shared__ float wred[kPrRows][kPrThreads / kWave];
+  PrioWork w;
+  if (!prio_work(a, w)) return;
+  const float* rowp[kPrRows];
 #pragma unroll
-  for (int r = 0; r < J; ++r) pf[r] = prot[min(p0 + (int)threadIdx.x + kPrThreads * r, ns - 1)];
-  prio_stage<kPrRows>(a, lh0, seq0, ns, p0, am);
+  for (int i = 0; i < kPrRows; ++i)
+    rowp[i] = a.sal + (size_t)min(w.lh0 + i, a.LH - 1) * a.ntot + w.seq0;
+  prio_stage(a, rowp, a.prot + w.seq0, w.ns, w.p0, st);
   __syncthreads();
+  constexpr int J = kPrChunk / kPrThreads;
 #pragma unroll
   for (int i = 0; i < kPrRows; ++i) {
-    float m = 0.f;  // U >= 0
+    float m = 0.f;  // U >= 0; positions past the sequence are not prunable in pf
 #pragma unroll
     for (int r = 0; r < J; ++r) {
       const int e = threadIdx.x + kPrThreads * r;
-      if (p0 + e < ns && pf[r] == 0) m = fmaxf(m, prio_pool<HALF>(am[i], e, a.half));
+      if (st.pf[e + a.half]) m = fmaxf(m, prio_pool<HALF>(st.am[i], e, a.half));
     }
     m = wave_max(m);
     if ((threadIdx.x & 63) == 0) wred[i][threadIdx.x >> 6] = m;
   }
   __syncthreads();
-  if (threadIdx.x < kPrRows && lh0 + (int)threadIdx.x < a.LH) {
+  if (threadIdx.x < kPrRows && w.lh0 + (int)threadIdx.x < a.LH) {
     const int i = threadIdx.x;
     float mm = 0.f;
-    for (int w = 0; w < kPrThreads / kWave; ++w) mm = fmaxf(mm, wred[i][w]);
-    a.scores[(size_t)(lh0 + i) * a.ntot + seq0 + p0] = mm;
+    for (int k = 0; k < kPrThreads / kWave; ++k) mm = fmaxf(mm, wred[i][k]);
+    a.scores[(size_t)(w.lh0 + i) * a.ntot + w.seq0 + w.p0] = mm;
   }
 }
 
@@ -645,52 +689,55 @@ __global__ __launch_bounds__(kWave) void prio_row_max_kernel(FuseArgs a) {
 
 template <int HALF, bool FLAGS>
 __global__ __launch_bounds__(kPrThreads) void prio_chunk_fuse_kernel(FuseArgs a) {
-  __shared__ float am[kPrRows][kPrChunk + 2 * kMaxHalf];
-  const int rgrp = blockIdx.x / a.total_chunks, g = blockIdx.x - rgrp * a.total_chunks;
-  const int lh0 = rgrp * kPrRows;
-  int s, c;
-  locate_chunk(a.cu_seqlens, a.S, g, s, c);
-  s = uniform(s);
-  if (s < 0) return;
-  const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
-  const int p0 = uniform(c) * kPrChunk;
-  const uint8_t* prot = a.prot + seq0;
-  const int32_t* sid = a.step_ids + seq0;
+  static_assert(kPrRows == 2, "the fuse loop is written for two rows");
+  __shared__ PrioStage st;
+  PrioWork w;
+  if (!prio_work(a, w)) return;
+  const float* rowp[kPrRows];
+  float* outp[kPrRows];
   float M[kPrRows];  // each row's maximum; read before the barrier below
 #pragma unroll
-  for (int i = 0; i < kPrRows; ++i)
-    M[i] = lh0 + i < a.LH ? a.scores[(size_t)(lh0 + i) * a.ntot + seq0 + p0] : 0.f;
-  const int st0 = a.cu_steps[s], nsteps = a.cu_steps[s + 1] - st0;
-  constexpr int J = kPrChunk / kPrThreads;
-  int32_t kv[J];  // step ids and protected flags of this thread's positions
-  uint32_t pf[J];
-#pragma unroll
-  for (int r = 0; r < J; ++r) {
-    const int p = min(p0 + (int)threadIdx.x + kPrThreads * r, ns - 1);
-    kv[r] = sid[p];
-    pf[r] = prot[p];
+  for (int i = 0; i < kPrRows; ++i) {
+    const size_t row = (size_t)min(w.lh0 + i, a.LH - 1) * a.ntot + w.seq0;
+    rowp[i] = a.sal + row;
+    outp[i] = a.scores + row;
+    M[i] = outp[i][w.p0];
   }
-  prio_stage<kPrRows>(a, lh0, seq0, ns, p0, am);
+  const int st0 = uniform(a.cu_steps[w.s]), nsteps = uniform(a.cu_steps[w.s + 1]) - st0;
+  const int32_t* sid = a.step_ids + w.seq0;
+  const float* util = a.util + st0;
+  constexpr int J = kPrChunk / kPrThreads;
+  const int nout = min(kPrChunk, w.ns - w.p0);  // positions of this chunk
+  int32_t kv[J];  // step ids of this thread's positions
+#pragma unroll
+  for (int r = 0; r < J; ++r) kv[r] = sid[w.p0 + min((int)threadIdx.x + kPrThreads * r, nout - 1)];
+  prio_stage(a, rowp, a.prot + w.seq0, w.ns, w.p0, st);
   __syncthreads();  // every thread has the maxima before position p0 takes its P
+  float inv[kPrRows];
+#pragma unroll
+  for (int i = 0; i < kPrRows; ++i) inv[i] = M[i] > 0.f ? 1.0f / M[i] : 0.f;
+  const bool two = w.lh0 + 1 < a.LH;  // uniform: the group's second row exists
   uint32_t bad = 0u;
 #pragma unroll
   for (int r = 0; r < J; ++r) {
-    const int e = threadIdx.x + kPrThreads * r, p = p0 + e;
-    if (p < ns) {
-      const bool pr = pf[r] == 0;
+    const int e = threadIdx.x + kPrThreads * r;
+    if (e < nout) {
+      const bool pr = st.pf[e + a.half] != 0;
       const int kk = kv[r];
-      const bool ok = pr && kk >= 0 && kk < nsteps;
-      const float util = ok ? a.util[st0 + kk] : 0.f;
-      if (FLAGS) bad |= pr && !ok ? kFlagStepId : 0u;
-#pragma unroll
-      for (int i = 0; i < kPrRows; ++i) {
-        if (lh0 + i >= a.LH) break;
-        const float inv = M[i] > 0.f ? 1.0f / M[i] : 0.f;
-        const float th = prio_pool<HALF>(am[i], e, a.half) * inv;
-        const float pv = pr ? fmaf(a.alpha, th, a.beta * util) : -INFINITY;
-        if (FLAGS) bad |= pr && !finite(pv) ? kFlagNonFinite : 0u;
-        a.scores[(size_t)(lh0 + i) * a.ntot + seq0 + p] = pv;
+      const bool ok = pr && (uint32_t)kk < (uint32_t)nsteps;
+      const float bu = a.beta * (ok ? util[kk] : 0.f);  // as the per-sequence kernels
+      const int p = w.p0 + e;
+      const float pv0 = pr ? fmaf(a.alpha, prio_pool<HALF>(st.am[0], e, a.half) * inv[0], bu)
+                           : -INFINITY;
+      outp[0][p] = pv0;
+      float pv1 = 0.f;
+      if (two) {
+        pv1 = pr ? fmaf(a.alpha, prio_pool<HALF>(st.am[1], e, a.half) * inv[1], bu) : -INFINITY;
+        outp[1][p] = pv1;
       }
+      if (FLAGS)
+        bad |= (pr && !ok ? kFlagStepId : 0u) |
+               (pr && !(finite(pv0) && finite(pv1)) ? kFlagNonFinite : 0u);
     }
   }
   if (FLAGS) report_flags(a.status, bad);
