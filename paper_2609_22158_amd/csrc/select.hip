@@ -15,7 +15,8 @@
 //
 // Sequences of up to 32768 tokens keep their keys in registers (32 per
 // thread, position tid + 1024 j in slot j); longer ones re-read the scores
-// in every pass. The work per key is plain VALU arithmetic over lane data;
+// in every pass. In a batch of 2 to 64 sequences the workgroups take the
+// rows of the longest sequences first. The work per key is plain VALU arithmetic over lane data;
 // per-slot lane masks are made where they are used, never held across a
 // phase, since 32 of them do not fit the scalar registers.
 #include "common.h"
@@ -205,12 +206,38 @@ struct RowSetup {
   int32_t* kept;
 };
 
+// Rows of the sequence of rank q when the sequences are ordered by decreasing
+// length (equal lengths by index), for batches of 2 to 64 sequences:
+// workgroups are dispatched in block order, so the rows of the longest
+// sequences start first and the shortest fill the end of the launch. Every
+// wave computes it from one round of loads of the sequence offsets.
+__device__ __forceinline__ void longest_first(const SelectArgs& a, int q, RowSetup& r) {
+  const int lane = threadIdx.x & 63;
+  const bool in = lane < a.S;
+  const int c0 = in ? a.cu_seqlens[lane] : 0;
+  const int len = in ? a.cu_seqlens[lane + 1] - c0 : -1;
+  int rank = 0;
+  for (int j = 0; j < a.S; ++j) {
+    const int lj = __shfl(len, j, kWave);
+    rank += (lj > len || (lj == len && j < lane)) ? 1 : 0;
+  }
+  // ranks are a permutation of 0 .. S-1
+  r.s = uniform(__builtin_ctzll(ballot(in && rank == q)));
+  r.seq0 = uniform(__shfl(c0, r.s, kWave));
+  r.ns = uniform(__shfl(len, r.s, kWave));
+}
+
 __device__ __forceinline__ RowSetup row_setup(const SelectArgs& a) {
   RowSetup r;
-  r.s = blockIdx.x / a.LH;
-  r.lh = blockIdx.x - r.s * a.LH;
-  r.seq0 = a.cu_seqlens[r.s];
-  r.ns = a.cu_seqlens[r.s + 1] - r.seq0;
+  const int q = blockIdx.x / a.LH;
+  r.lh = blockIdx.x - q * a.LH;
+  if (a.S > 1 && a.S <= kWave) {
+    longest_first(a, q, r);
+  } else {
+    r.s = q;
+    r.seq0 = a.cu_seqlens[r.s];
+    r.ns = a.cu_seqlens[r.s + 1] - r.seq0;
+  }
   r.B = a.budgets ? max(1, a.budgets[r.s]) : a.budget;
   const int st0 = a.kept ? a.cu_steps[r.s] : 0;
   r.nsteps = a.kept ? a.cu_steps[r.s + 1] - st0 : 0;
@@ -289,6 +316,26 @@ __device__ __forceinline__ void write_retained(const SelectArgs& a, int s, int b
   }
 }
 
+// The M-th largest candidate key among a thread's slots, 0 when it holds
+// fewer than M candidates (candidate keys are never 0).
+template <int M>
+__device__ __forceinline__ uint32_t mth_largest(const uint32_t (&keys)[kCached]) {
+  uint32_t top[M];  // the largest so far, in descending order
+#pragma unroll
+  for (int q = 0; q < M; ++q) top[q] = 0u;
+#pragma unroll
+  for (int j = 0; j < kCached; ++j) {
+    uint32_t x = keys[j] - 1u < kProtKey - 1u ? keys[j] : 0u;
+#pragma unroll
+    for (int q = 0; q < M; ++q) {
+      const uint32_t hi = max(top[q], x);
+      x = min(top[q], x);
+      top[q] = hi;
+    }
+  }
+  return top[M - 1];
+}
+
 // ---------------------------------------------------------------- N_s <= 32768
 __global__ __launch_bounds__(kThreads) void select_cached_kernel(SelectArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t hist[2 * kBins];
@@ -332,12 +379,21 @@ __global__ __launch_bounds__(kThreads) void select_cached_kernel(SelectArgs a) {
     kmin1 = min(kmin1, km);
     kmax1 = max(kmax1, keys[j] + 1u);  // kProtKey + 1 wraps to 0
   }
-  // A lower bound for tau: each thread holding a candidate has its largest
-  // candidate key (kmax1 - 1), so at least as many candidates as there are such
-  // threads lie at or above the smallest of those maxima; when ktake is within
-  // that number, tau lies there too and the search skips every key below it.
-  const bool has = kmax1 >= 2u;
-  uint32_t tmax = has ? kmax1 - 1u : 0xFFFFFFFFu;
+  // A lower bound for tau: each thread holding at least m candidates has m
+  // of them at or above its m-th largest, so at least m times as many
+  // candidates as there are such threads lie at or above the smallest of
+  // those m-th largest keys; when ktake is within that number, tau lies there
+  // too and the search skips every key below it. m = 1, 2 or 4, the least
+  // for which the budget can be within the bound.
+  const int m = r.B <= kThreads ? 1 : (r.B <= 2 * kThreads ? 2 : 4);
+  uint32_t mth;  // this thread's m-th largest candidate key, 0 with fewer than m
+  if (m == 1) {
+    mth = kmax1 >= 2u ? kmax1 - 1u : 0u;
+  } else {
+    mth = m == 2 ? mth_largest<2>(keys) : mth_largest<4>(keys);
+  }
+  const bool has = mth != 0u;
+  uint32_t tmax = has ? mth : 0xFFFFFFFFu;
   const int nthr = __popcll(ballot(has));  // wave total
   // count, key range and the bound, reduced in one barrier round; kmin1 and
   // kmax1 in the shifted domains, where non-candidates lose every min and max
@@ -373,7 +429,7 @@ __global__ __launch_bounds__(kThreads) void select_cached_kernel(SelectArgs a) {
   uint32_t tau = 0u;
   int need = 0;
   if (!take_all) {
-    const uint32_t lbound = ktake <= nthr_all ? tmax : kmin;  // tau >= lbound
+    const uint32_t lbound = ktake <= m * nthr_all ? tmax : kmin;  // tau >= lbound
     if (lbound == kmax) {
       tau = kmax;  // every candidate from the bound up ties
       need = ktake;
