@@ -310,14 +310,14 @@ def _special_scores(w, seed):
 
 @pytest.mark.parametrize("seqlens", [[2500, 700, 130, 1, 0, 4097, 32768], [40000, 3001]],
                          ids=["registers", "streamed"])
-@pytest.mark.parametrize("budget", [1, 37, 1000, 1500, 2048, 3000, 4096])
+@pytest.mark.parametrize("budget", [1, 37, 1000, 1024, 1025, 1500, 2048, 2049, 3000, 4096])
 def test_select_special_values_bitexact(seqlens, budget):
     """Selection on crafted fp32 priorities == the oracle's stable ranking of the same numbers
     (NaN as -inf, -0 as +0), including the kept-per-step counts; sequences up to 32768 tokens
     take the register path, longer ones the streamed path. The register path bounds tau from
     below by the smallest per-thread m-th largest key: m = 1 for budgets up to the 1024
-    threads (1, 37, 1000), 2 up to 2048 (1500, 2048) and 4 above (3000, 4096); where the
-    bound does not hold for a row it takes the full key range."""
+    threads (1, 37, 1000, 1024), 2 up to 2048 (1025, 1500, 2048) and 4 above (2049, 3000,
+    4096); where the bound does not hold for a row it takes the full key range."""
     import torch
 
     w = reduced("ragged16", num_layers=2, seqlens=seqlens, protected_len=64, with_v=False)
