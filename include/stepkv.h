@@ -95,6 +95,10 @@ extern "C" {
                                     step_utility); its priority is not finite */
 #define STEPKV_FLAG_OUT_ROWS 4u  /* cu_retained[S] exceeded out_rows: rows at or past
                                     out_rows were not written (compact) or read (decode) */
+#define STEPKV_FLAG_SYNC 8u      /* a column-sum workgroup of the one-launch saliency
+                                    sweeps stopped waiting for its (sequence, head)'s row
+                                    LSEs after its poll bound: that head's saliency and
+                                    scores are not valid (not expected to occur) */
 
 /* ---------------------------------------------------------------- types */
 /* Shape of one compression problem: a batch of S sequences, all layers. */
@@ -348,7 +352,7 @@ int stepkv_score(const stepkv_problem* pb, const stepkv_params* prm, const void*
  * which keeps the last call's contents (no part of it needs to start at
  * zero): calls that overlap on one GPU, on different streams or threads,
  * race and must be ordered by the caller. */
-#define STEPKV_STATIC_SCRATCH_BYTES ((size_t)32 << 20)
+#define STEPKV_STATIC_SCRATCH_BYTES ((size_t)128 << 20)
 int stepkv_score_noalloc(const stepkv_problem* pb, const stepkv_params* prm, const void* q_win,
                          const void* k, const int32_t* step_ids, const uint8_t* protected_mask,
                          const float* step_utility, float* scores, float* saliency,

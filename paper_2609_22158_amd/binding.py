@@ -16,8 +16,8 @@ import numpy as np
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstepkv.so")
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP, ESCRATCH = 0, -1, -2, -3, -4, -5
-STATIC_SCRATCH_BYTES = 32 << 20  # STEPKV_STATIC_SCRATCH_BYTES
-FLAG_STEP_ID, FLAG_NONFINITE, FLAG_OUT_ROWS = 1, 2, 4  # STEPKV_FLAG_*
+STATIC_SCRATCH_BYTES = 128 << 20  # STEPKV_STATIC_SCRATCH_BYTES
+FLAG_STEP_ID, FLAG_NONFINITE, FLAG_OUT_ROWS, FLAG_SYNC = 1, 2, 4, 8  # STEPKV_FLAG_*
 CUE_CAP = 64  # STEPKV_CUE_CAP
 MAX_WINDOW_ROWS = 2048
 MAX_POOL_KERNEL = 63

@@ -22,6 +22,18 @@ constexpr size_t kAlign = 256;
 // about as long as six key tiles.
 constexpr int kSalSlots = 2 * 256;
 constexpr int kSalStartTiles = 6;
+// Both saliency sweeps in one launch (stepkv_score and the shared-index
+// scoring): a (sequence, head)'s column-sum chunks start about one round of
+// resident workgroups after its row-LSE chunks, and the K that the row-LSE
+// chunks in between read from HBM has to fit the 256 MB Infinity Cache
+// beside it for the second read of the chunk to hit there. Shorter chunks
+// keep that window smaller but start more workgroups; 192 MiB (about 2300-key
+// chunks at d = 128) measured best on the 32k, 16k, ragged and last-query
+// workloads.
+#ifndef STEPKV_SAL_FUSED
+#define STEPKV_SAL_FUSED 1
+#endif
+constexpr int64_t kFusedReuseBytes = int64_t(192) << 20;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -62,6 +74,8 @@ int max_seqlen(const stepkv_problem* pb) {
 
 struct SaliencyPlan {
   int R, rows_pad, chunk, total_chunks;
+  // both sweeps in one launch: chunk, chunk count and row-LSE lead (items)
+  int fused_chunk, fused_total_chunks, fused_lag;
 };
 
 // Window rows per pair of sweeps (the MFMA tiling holds at most 256).
@@ -96,11 +110,30 @@ SaliencyPlan plan_saliency(const stepkv_problem* pb) {
     }
   }
   p.total_chunks = (int)chunks_for(p.chunk);
+  // One launch of both sweeps: the longest chunk (a multiple of 128 keys) whose
+  // lead keeps the K read between a chunk's two sweeps within kFusedReuseBytes.
+  // The lead is half the resident workgroups (the item order alternates the
+  // sweeps) plus a sequence's chunks (its last row-LSE chunk comes that much
+  // later) plus an eighth of the workgroups as margin; it is also at least a
+  // sequence's chunk count, which orders every column-sum chunk after all
+  // row-LSE chunks of its (sequence, head).
+  auto most_chunks = [&](int c) {
+    int m = 0;
+    for (int s = 0; s < pb->num_seqs; ++s)
+      m = std::max(m, (pb->cu_seqlens_host[s + 1] - pb->cu_seqlens_host[s] + c - 1) / c);
+    return m;
+  };
+  auto lead = [&](int c) { return (int64_t)kSalSlots / 2 + most_chunks(c) + kSalSlots / 8; };
+  p.fused_chunk = 128;
+  for (int c = 128; c <= 4096; c += 128)
+    if (lead(c) * c * 2 * pb->head_dim <= kFusedReuseBytes) p.fused_chunk = c;
+  p.fused_total_chunks = (int)chunks_for(p.fused_chunk);
+  p.fused_lag = (int)std::min<int64_t>(lead(p.fused_chunk), lh * p.fused_total_chunks);
   return p;
 }
 
 struct WsLayout {
-  size_t partial, lse, sal, total;
+  size_t partial, lse, cnt, sal, total;
 };
 
 WsLayout layout(const stepkv_problem* pb, const SaliencyPlan& p) {
@@ -108,10 +141,13 @@ WsLayout layout(const stepkv_problem* pb, const SaliencyPlan& p) {
   const size_t ntot = (size_t)pb->cu_seqlens_host[pb->num_seqs];
   WsLayout w;
   size_t off = 0;
-  w.partial = off;
-  off = align_up(off + sizeof(float) * 2 * lh * p.total_chunks * p.rows_pad);
+  w.partial = off;  // sized for the longer chunk list of the two plans
+  off = align_up(off + sizeof(float) * 2 * lh *
+                           std::max(p.total_chunks, p.fused_total_chunks) * p.rows_pad);
   w.lse = off;
   off = align_up(off + sizeof(float) * pb->num_seqs * lh * p.rows_pad);
+  w.cnt = off;  // per (sequence, head) counters of the one-launch sweeps
+  off = align_up(off + sizeof(int32_t) * pb->num_seqs * lh);
   w.sal = off;
   off = align_up(off + sizeof(float) * lh * ntot);
   w.total = off;
@@ -280,8 +316,12 @@ int run_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void*
   sa.Hkv = pb->num_kv_heads;
   sa.G = pb->num_q_heads / pb->num_kv_heads;
   sa.ntot = pb->cu_seqlens_host[pb->num_seqs];
-  sa.chunk = plan.chunk;
-  sa.total_chunks = plan.total_chunks;
+  sa.status = pb->status;
+  const bool fused = STEPKV_SAL_FUSED != 0 && mode == SaliencyMode::kBoth;
+  sa.chunk = fused ? plan.fused_chunk : plan.chunk;
+  sa.total_chunks = fused ? plan.fused_total_chunks : plan.total_chunks;
+  sa.unit_cnt = fused ? reinterpret_cast<int*>(ws + w.cnt) : nullptr;
+  sa.lag = plan.fused_lag;
   const double scale = prm->scale > 0.0f ? (double)prm->scale : 1.0 / std::sqrt((double)d);
   sa.c = (float)(scale * 1.4426950408889634);  // log2(e)
   // Window rows in groups of at most 256, one pair of sweeps per group: a

@@ -27,6 +27,12 @@ struct SaliencyArgs {
   int ntot, chunk, total_chunks;
   int causal;  // nonzero: window slot w sees keys 0 .. N_s - W + w only
   float c;     // softmax scale * log2(e)
+  // both sweeps in one launch (saliency_fused_kernel) when set: per (sequence,
+  // head) counters [S][L*Hkv], cleared by the launcher; lag = row-LSE items
+  // ahead of the column-sum items
+  int* unit_cnt;
+  int lag;
+  uint32_t* status;  // device status word (STEPKV_FLAG_*) or null
 };
 
 // Rows padded to whole row groups: 64, 128 or 256.
@@ -118,11 +124,11 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int n, hipStream_t st);
 
 // The static device scratch of stepkv_score_noalloc (STEPKV_STATIC_SCRATCH_BYTES):
 // its address on the current device, looked up on the first call per device.
-constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+constexpr size_t kStaticScratchBytes = size_t(128) << 20;
 hipError_t static_scratch(void** ptr);
 
 // Device status bits (the STEPKV_FLAG_* values of stepkv.h).
-constexpr uint32_t kFlagStepId = 1u, kFlagNonFinite = 2u, kFlagOutRows = 4u;
+constexpr uint32_t kFlagStepId = 1u, kFlagNonFinite = 2u, kFlagOutRows = 4u, kFlagSync = 8u;
 
 // ---------------------------------------------------------------- decode check
 struct DecodeArgs {

@@ -52,6 +52,12 @@ __device__ __forceinline__ int tile_offset(int r, int p) {
 #ifndef STEPKV_SAL_SYNC_TILES
 #define STEPKV_SAL_SYNC_TILES 2
 #endif
+// With one barrier per two tiles: read the K fragments of tile t+2 while the
+// MFMAs of tile t+1 run (each fragment register is refilled right after its
+// last MFMA), so that no tile starts on an LDS round trip.
+#ifndef STEPKV_SAL_FRAG_AHEAD
+#define STEPKV_SAL_FRAG_AHEAD 1
+#endif
 
 // One 16-byte LDS read of the K ring at addr + OFF. Issued as assembly so
 // that the compiler, which cannot tell the ring slots apart, does not put a
@@ -155,23 +161,78 @@ __host__ __device__ __forceinline__ void static_for(F&& f) {
 // compile-time LDS offset: fragment reads use per-lane addresses computed
 // once plus an immediate, and full tiles load from a scalar base plus
 // per-lane constant offsets.
-template <int D, int RG, int PASS, bool CAUSAL>
-__global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
-  constexpr int KG = 4 / RG;
-  constexpr int TILE = 32 * KG;               // keys per workgroup iteration
-  constexpr int KSTEPS = D / 16;              // MFMA k-steps
-  constexpr int TILE_BYTES = TILE * 2 * D;
+// Device-coherent accesses (relaxed atomics at agent scope: they bypass the
+// per-XCD L2) for the few values that one workgroup of the one-launch sweeps
+// hands to another: the chunk partials, the row LSEs and the counters. A
+// writer waits for its stores (vmcnt 0) before it moves a counter, and a
+// reader issues its loads after it has seen the counter, so no L2 write-back
+// or invalidation is needed around them.
+__device__ __forceinline__ void store_coherent(float2* p, float2 v) {
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), __builtin_bit_cast(uint64_t, v),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+  __hip_atomic_store(reinterpret_cast<uint32_t*>(p), __builtin_bit_cast(uint32_t, v),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 load_coherent(const float2* p) {
+  return __builtin_bit_cast(float2, __hip_atomic_load(reinterpret_cast<const uint64_t*>(p),
+                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+__device__ __forceinline__ float load_coherent(const float* p) {
+  return __builtin_bit_cast(float, __hip_atomic_load(reinterpret_cast<const uint32_t*>(p),
+                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+// This wave's stores have completed.
+__device__ __forceinline__ void stores_done() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Compile-time shape of the sweeps for head dim D and RG row groups: the K
+// ring (NBUF tiles of TILE keys) and the LDS buffers of the column partials.
+template <int D, int RG>
+struct SweepShape {
+  static constexpr int KG = 4 / RG;
+  static constexpr int TILE = 32 * KG;               // keys per workgroup iteration
+  static constexpr int KSTEPS = D / 16;              // MFMA k-steps
+  static constexpr int TILE_BYTES = TILE * 2 * D;
   // ring slots: an even count, 2 to 8, within STEPKV_SAL_RING_BYTES
-  constexpr int NBUF_FIT = STEPKV_SAL_RING_BYTES / TILE_BYTES;
-  constexpr int NBUF = NBUF_FIT >= 8 ? 8 : (NBUF_FIT >= 2 ? NBUF_FIT & ~1 : 2);
-  constexpr int NLD = TILE_BYTES / (kThreads * 16);  // 16-byte loads per thread per tile
+  static constexpr int NBUF_FIT = STEPKV_SAL_RING_BYTES / TILE_BYTES;
+  static constexpr int NBUF = NBUF_FIT >= 8 ? 8 : (NBUF_FIT >= 2 ? NBUF_FIT & ~1 : 2);
+  static constexpr int NLD = TILE_BYTES / (kThreads * 16);  // 16-byte loads per thread per tile
+  // tiles per workgroup barrier: 1, or 2 when the ring holds at least 4 tiles
+  static constexpr int SYNC = (STEPKV_SAL_SYNC_TILES == 2 && NBUF >= 4) ? 2 : 1;
+  static constexpr int NRED = 2 * SYNC;  // column-partial buffers of the second sweep
+  static constexpr int RING_BYTES = NBUF * TILE_BYTES;
+  static constexpr int RED_FLOATS = NRED * kThreads;
+};
+
+// One sweep over one key chunk: global chunk g (the chunks of all sequences in
+// order) of head lh, with the workgroup's K ring and partial buffers in LDS.
+// PASS 1 writes the chunk's per-row (max, sum) partials, PASS 2 the chunk's
+// column sums (from the row LSEs in a.lse2).
+// FUSED (both sweeps in one launch): the first sweep's K loads keep their
+// lines in the caches, where the second sweep reads the chunk again, and the
+// partials and row LSEs that pass between workgroups use device-coherent
+// accesses. Otherwise every K load is non-temporal, which leaves the caches to
+// the saliency the second sweep writes and the priority reads next.
+template <int D, int RG, int PASS, bool CAUSAL, bool FUSED, typename BeforeLse>
+__device__ __forceinline__ void sweep(const SaliencyArgs& a, int lh, const int rem_blk,
+                                      uint8_t* __restrict__ kbuf, float* __restrict__ red,
+                                      BeforeLse&& before_lse) {
+  using Sh = SweepShape<D, RG>;
+  constexpr int KG = Sh::KG;
+  constexpr int TILE = Sh::TILE;
+  constexpr int KSTEPS = Sh::KSTEPS;
+  constexpr int TILE_BYTES = Sh::TILE_BYTES;
+  constexpr int NBUF = Sh::NBUF;
+  constexpr int NLD = Sh::NLD;
   static_assert(NLD >= 1, "tile too small");
   static_assert((NBUF - 1) * TILE_BYTES < 65536, "ring offset must fit the ds_read offset field");
-  // tiles per workgroup barrier: 1, or 2 when the ring holds at least 4 tiles
-  constexpr int SYNC = (STEPKV_SAL_SYNC_TILES == 2 && NBUF >= 4) ? 2 : 1;
-  constexpr int NRED = 2 * SYNC;  // column-partial buffers of the second sweep
-  __shared__ __attribute__((aligned(16))) uint8_t kbuf[NBUF * TILE_BYTES];
-  __shared__ float red[NRED * kThreads];
+  constexpr int SYNC = Sh::SYNC;
+  // fragments one tile ahead (needs the two-tile barrier: a barrier at even
+  // tile t makes tiles t+2 and t+3 visible, read in bodies t and t+1)
+  constexpr bool AHEAD = SYNC == 2 && (STEPKV_SAL_FRAG_AHEAD == 2 ||
+                                        (STEPKV_SAL_FRAG_AHEAD == 1 && PASS == 1 && RG == 4 && !CAUSAL));
+  constexpr int NRED = Sh::NRED;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -181,9 +242,6 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
 
   // ---- work item: (head lh, sequence s, chunk c)
   const int LH = a.L * a.Hkv;
-  int lh = blockIdx.x / a.total_chunks;
-  const int rem_blk = blockIdx.x - lh * a.total_chunks;
-  if (PASS == 2) lh = LH - 1 - lh;  // pass 2 starts where pass 1 ended (cache reuse)
   int s, cfirst;
   locate_chunk(a, rem_blk, s, cfirst);
   s = uniform(s);
@@ -195,25 +253,6 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   const int nkeys = min(a.chunk, ns - key0);
   const int ntiles = (nkeys + TILE - 1) / TILE;
   const uint16_t* __restrict__ kseq = a.k + ((size_t)lh * a.ntot + seq0) * D;
-
-  // ---- window rows of this wave: two 32-row blocks of the launch's row group
-  // (rows row0 + local row), k-slices (D/2)*hf + 8*st
-  bf16x8_t qf[2][KSTEPS];
-#pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int row = rg * 64 + b * 32 + col;
-    if (row < a.R) {
-      const int w = (a.row0 + row) / a.G, g = (a.row0 + row) - w * a.G;
-      const uint16_t* qp =
-          a.q + ((((size_t)l * a.S + s) * a.W + w) * a.Hq + h * a.G + g) * D + (D / 2) * hf;
-#pragma unroll
-      for (int st = 0; st < KSTEPS; ++st)
-        qf[b][st] = *reinterpret_cast<const bf16x8_t*>(qp + 8 * st);
-    } else {
-#pragma unroll
-      for (int st = 0; st < KSTEPS; ++st) qf[b][st] = bf16x8_t{};
-    }
-  }
 
   // ---- K ring: this lane's 16-byte pieces of a tile (HBM side) ...
   const char* __restrict__ kbytes = reinterpret_cast<const char*>(kseq);
@@ -246,7 +285,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
         __builtin_amdgcn_global_load_lds(static_cast<const void*>(tb + ld_off[j]),
                                          (__attribute__((address_space(3))) void*)(
                                              base + 16 * (kThreads * j + 64 * wave)),
-                                         16, 0, 0);
+                                         16, 0, FUSED && PASS == 1 ? 0 : 2);
     } else {  // tail rows re-read the last valid key
 #pragma unroll
       for (int j = 0; j < NLD; ++j) {
@@ -255,7 +294,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
         __builtin_amdgcn_global_load_lds(static_cast<const void*>(src),
                                          (__attribute__((address_space(3))) void*)(
                                              base + 16 * (kThreads * j + 64 * wave)),
-                                         16, 0, 0);
+                                         16, 0, FUSED && PASS == 1 ? 0 : 2);
       }
     }
   };
@@ -264,6 +303,37 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
 #pragma unroll
     for (int st = 0; st < KSTEPS; ++st) kf[st] = lds_read_b128<slot * TILE_BYTES>(fa[st]);
   };
+
+  // The first K tiles go out before the window rows of Q, so that a chunk
+  // starts after one memory round trip, not two. With fragments one tile ahead
+  // every slot fills now (tiles 0 and 1 must land), otherwise all but the last
+  // (it fills at tile 0's barrier, or below with one barrier per tile).
+  static_for<0, AHEAD ? NBUF : NBUF - 1>([&](auto ic) __attribute__((always_inline)) {
+    if (decltype(ic)::value < ntiles) issue_tile(decltype(ic)::value, ic);
+  });
+
+  // ---- window rows of this wave: two 32-row blocks of the launch's row group
+  // (rows row0 + local row), k-slices (D/2)*hf + 8*st
+  bf16x8_t qf[2][KSTEPS];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int row = rg * 64 + b * 32 + col;
+    if (row < a.R) {
+      const int w = (a.row0 + row) / a.G, g = (a.row0 + row) - w * a.G;
+      const uint16_t* qp =
+          a.q + ((((size_t)l * a.S + s) * a.W + w) * a.Hq + h * a.G + g) * D + (D / 2) * hf;
+#pragma unroll
+      for (int st = 0; st < KSTEPS; ++st)
+        qf[b][st] = *reinterpret_cast<const bf16x8_t*>(qp + 8 * st);
+    } else {
+#pragma unroll
+      for (int st = 0; st < KSTEPS; ++st) qf[b][st] = bf16x8_t{};
+    }
+  }
+
+  // the caller's step before the row LSEs are read (the wait of a column-sum
+  // chunk for its head's row LSEs in the one-launch sweeps)
+  before_lse();
 
   // pass 1 state: per lane and row block, a log2-domain reference m2 and the
   // sum of exp2(c z - m2) over the keys seen so far (the pair stands for
@@ -278,7 +348,10 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) lr[b][j] = lp[b * 32 + 8 * (j >> 2) + 4 * hf + (j & 3)];
+      for (int j = 0; j < 16; ++j) {
+        const float* e = lp + b * 32 + 8 * (j >> 2) + 4 * hf + (j & 3);
+        lr[b][j] = FUSED ? load_coherent(e) : *e;
+      }
   }
 
 #pragma unroll
@@ -400,6 +473,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   // NB: row blocks of this wave that hold window rows (2, or 1 when the second
   // is padding past R: its MFMAs and softmax work are skipped; the result is
   // the same, as padding rows contribute exact zeros)
+  bf16x8_t kf[KSTEPS];  // K fragments of the tile whose MFMAs run next
   auto body = [&](auto ic, int t, f32x16_t(&cur)[2], f32x16_t(&nxt)[2], auto nb_c) __attribute__((always_inline)) {
     constexpr int i = decltype(ic)::value;
     constexpr int NB = decltype(nb_c)::value;
@@ -410,6 +484,15 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
       wait_tiles<NLD, NBUF - 2>(min(NBUF - 2, ntiles - 2 - t));
       lds_barrier();
       if (t + NBUF < ntiles) issue_tile(t + NBUF, ic);  // into the slot tile t has left
+    } else if constexpr (i % 2 == 0 && AHEAD) {
+      // one barrier per two tiles, fragments one tile ahead: tiles t+2 and t+3
+      // have landed (those that exist); every wave holds tile t+1's fragments
+      // (read in the body before), so the slots of tiles t and t+1 take new tiles
+      wait_tiles<NLD, NBUF - 4>(max(0, min(NBUF - 4, ntiles - 4 - t)));
+      lds_barrier();
+      if (t + NBUF < ntiles) issue_tile(t + NBUF, ic);
+      if (t + NBUF + 1 < ntiles)
+        issue_tile(t + NBUF + 1, std::integral_constant<int, (i + 1) % NBUF>{});
     } else if constexpr (i % 2 == 0) {
       // one barrier per two tiles: tiles t+1 and t+2 have landed (t+2 when it
       // exists); after the barrier every wave is done with tiles t-1 and t, so
@@ -427,8 +510,14 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     int rt = -1;       // tile whose partials this wave sums
     int rtid = TILE;   // its key within that tile (>= TILE: none)
     if constexpr (RED_HERE) {
+      // per two tiles: rotated thread index ra < TILE sums tile t-2 (key ra);
+      // the threads with ra in [256 - SHIFT, 256 - SHIFT + TILE) sum tile t-1
+      // (key rb = ra + SHIFT - 256): another wave for tiles of up to 64 keys,
+      // the other half of the threads for 128-key tiles
+      constexpr int SHIFT = TILE <= 64 ? 64 : 128;
+      static_assert(SYNC == 1 || TILE <= 128, "two tiles per barrier need 2 * TILE <= 256 threads");
       const int ra = (tid + 64 * i) & (kThreads - 1);
-      const int rb = (tid + 64 * (i + 1)) & (kThreads - 1);
+      const int rb = (ra + SHIFT) & (kThreads - 1);
       if (SYNC == 1) {
         rt = t - 1;
         rtid = ra;
@@ -451,8 +540,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
         part[2 * r2 + 1] = rp[(kg2 * RG + r2) * 64 + 32 + col2];
       }
     }
-    bf16x8_t kf[KSTEPS];
-    read_frags(std::integral_constant<int, (i + 1) % NBUF>{}, kf);
+    if constexpr (!AHEAD) read_frags(std::integral_constant<int, (i + 1) % NBUF>{}, kf);
     if (tile_has_hidden(t)) mask_hidden(cur, t);
     __builtin_amdgcn_sched_barrier(0);
     nxt[0] = f32x16_t{};
@@ -497,7 +585,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     static_for<0, NSL>([&](auto i2c) __attribute__((always_inline)) {
       constexpr int i2 = decltype(i2c)::value;
       constexpr int st = NB == 2 ? i2 >> 1 : i2, b = NB == 2 ? i2 & 1 : 0;
-      if constexpr (b == 0) lds_wait<KSTEPS - 1 - st>(kf[st]);
+      if constexpr (b == 0 && !AHEAD) lds_wait<KSTEPS - 1 - st>(kf[st]);
       if (PASS == 1)
         nxt[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qf[b][st], nxt[b], 0, 0, 0);
       else
@@ -506,11 +594,18 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
       if constexpr (i2 >= 2) stage_sum(std::integral_constant<int, i2 - 2>{});
       if constexpr (i2 >= 1) stage_exp(std::integral_constant<int, i2 - 1>{});
       stage_logit(i2c);
+      // the register of fragment st is free after its last MFMA: refill it with
+      // tile t+2's fragment (a stale slot when t+2 is past the chunk; never used)
+      if constexpr (AHEAD && b == NB - 1)
+        kf[st] = lds_read_b128<((i + 2) % NBUF) * TILE_BYTES>(fa[st]);
       __builtin_amdgcn_sched_barrier(0);
     });
     stage_exp(std::integral_constant<int, NSL - 1>{});
     stage_sum(std::integral_constant<int, NSL - 2>{});
     stage_sum(std::integral_constant<int, NSL - 1>{});
+    // tile t+2's fragments are complete before any branch: a value still in
+    // flight must not reach code where the compiler may copy its register
+    if constexpr (AHEAD) lds_settle(kf);
     // every partial sum is formed here, inside the MFMA sequence: without this
     // the compiler sinks block 1's work past block 0's branch below
     if constexpr (NB == 1) {
@@ -565,19 +660,20 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
     }
   };
 
-  static_for<0, NBUF - 1>([&](auto ic) __attribute__((always_inline)) {
-    if (decltype(ic)::value < ntiles) issue_tile(decltype(ic)::value, ic);
-  });
-  wait_tiles<NLD, NBUF - 2>(min(NBUF - 2, ntiles - 1));  // tile 0 has landed
+  if constexpr (AHEAD)
+    wait_tiles<NLD, NBUF - 2>(max(0, min(NBUF - 2, ntiles - 2)));  // tiles 0 and 1 have landed
+  else
+    wait_tiles<NLD, NBUF - 2>(min(NBUF - 2, ntiles - 1));  // tile 0 has landed
   lds_barrier();
-  // one barrier per tile: the last slot fills now; per two tiles: at tile 0's barrier
   if (SYNC == 1 && NBUF - 1 < ntiles) issue_tile(NBUF - 1, std::integral_constant<int, NBUF - 1>{});
   f32x16_t acc_a[2], acc_b[2];
-  {
-    bf16x8_t kf[KSTEPS];
-    read_frags(std::integral_constant<int, 0>{}, kf);
+  read_frags(std::integral_constant<int, 0>{}, kf);
+  lds_settle(kf);
+  mfma_tile(kf, acc_a);
+  // tile 1's fragments for the first body (a stale slot when there is no tile 1)
+  if constexpr (AHEAD) {
+    read_frags(std::integral_constant<int, 1>{}, kf);
     lds_settle(kf);
-    mfma_tile(kf, acc_a);
   }
   if (PASS == 1 && ntiles > 1) {  // tile 0 is full: its maxima are the first references
     if (tile_has_hidden(0)) mask_hidden(acc_a, 0);
@@ -671,15 +767,166 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   if (kg == 0 && hf == 0) {
     float2* out = a.partial + ((size_t)lh * a.total_chunks + rem_blk) * a.rows_pad;
 #pragma unroll
-    for (int b = 0; b < 2; ++b) out[rg * 64 + b * 32 + col] = make_float2(m2[b], zs[b]);
+    for (int b = 0; b < 2; ++b) {
+      float2* e = out + rg * 64 + b * 32 + col;
+      if (FUSED) store_coherent(e, make_float2(m2[b], zs[b]));
+      else *e = make_float2(m2[b], zs[b]);
+    }
+  }
+}
+
+// One launch per sweep: block b takes chunk b % total_chunks of head
+// b / total_chunks (the column-sum sweep walks the heads in reverse, so that
+// it starts on the heads the row-LSE sweep read last).
+template <int D, int RG, int PASS, bool CAUSAL>
+__global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
+  using Sh = SweepShape<D, RG>;
+  __shared__ __attribute__((aligned(16))) uint8_t kbuf[Sh::RING_BYTES];
+  __shared__ float red[Sh::RED_FLOATS];
+  const int LH = a.L * a.Hkv;
+  int lh = blockIdx.x / a.total_chunks;
+  const int g = blockIdx.x - lh * a.total_chunks;
+  if (PASS == 2) lh = LH - 1 - lh;
+  sweep<D, RG, PASS, CAUSAL, false>(a, lh, g, kbuf, red, [] {});
+}
+
+// The log2-domain row LSE from a row's merged (max, sum): +inf for padding
+// rows and rows that see no key (probability zero in the second sweep); the
+// natural-log value of every real row is exported when lse_out is set (-inf
+// for a row that sees no key).
+template <bool COHERENT>
+__device__ __forceinline__ void store_row_lse(const SaliencyArgs& a, int s, int lh, int row,
+                                              float M, float Z) {
+  const int LH = a.L * a.Hkv;
+  const bool seen = row < a.R && Z > 0.f;
+  const float l2 = seen ? M + log2f(Z) : INFINITY;
+  float* e = a.lse2 + ((size_t)s * LH + lh) * a.rows_pad + row;
+  if (COHERENT) store_coherent(e, l2);
+  else *e = l2;
+  if (a.lse_out && row < a.R) {
+    const int l = lh / a.Hkv, h = lh - l * a.Hkv;
+    const int w = (a.row0 + row) / a.G, g = (a.row0 + row) - w * a.G;
+    a.lse_out[(((size_t)l * a.S + s) * a.W + w) * a.Hq + h * a.G + g] =
+        seen ? l2 * 0.693147180559945309f : -INFINITY;
+  }
+}
+
+// ---- both sweeps in one launch, K read once from HBM
+//
+// Work items are the chunks of both sweeps. The row-LSE items of every
+// (sequence, head) come first in item order and its column-sum items follow
+// about one round of resident workgroups later, so that the K they read
+// again is still in the Infinity Cache: item t of the launch is
+//   t < lag:               row-LSE item t
+//   lag <= t < 2M - lag:   row-LSE item lag + (t - lag) / 2 (t - lag even),
+//                          column-sum item (t - lag - 1) / 2 (t - lag odd)
+//   t >= 2M - lag:         column-sum item t - M
+// with M items per sweep, in the order head-major, chunks of the sequences in
+// order. The column-sum item k follows the row-LSE items of its (sequence,
+// head) in this order when lag is at least the most chunks of a sequence.
+//
+// Each (sequence, head) has a counter: every row-LSE item adds one after its
+// partials have reached device-coherent memory; the one that completes the
+// count merges the partials into the row LSEs and adds one more. A column-sum item waits
+// for count = chunks + 1. Blocks start in index order, so every row-LSE item
+// a column-sum item waits for has started and finishes without waiting; the
+// wait is still bounded (kFusedSpins polls), and one that runs out sets
+// STEPKV_FLAG_SYNC in the status word and goes on.
+constexpr int kFusedSpins = 1 << 17;
+
+__device__ __forceinline__ void fused_item(int t, int M, int lag, int& pass, int& k) {
+  if (t < lag) {
+    pass = 1;
+    k = t;
+  } else if (t < 2 * M - lag) {
+    const int j = t - lag;
+    pass = (j & 1) ? 2 : 1;
+    k = (j & 1) ? (j >> 1) : lag + (j >> 1);
+  } else {
+    pass = 2;
+    k = t - M;
+  }
+}
+
+// Row LSEs of (s, lh) from the partials of its nch chunks from global chunk
+// c0 on: one thread per row, the chunks in order, eight loads in flight.
+__device__ __forceinline__ void merge_unit(const SaliencyArgs& a, int s, int lh, int c0,
+                                           int nch) {
+  const int row = threadIdx.x;
+  if (row >= a.rows_pad) return;
+  const float2* __restrict__ pp =
+      a.partial + ((size_t)lh * a.total_chunks + c0) * a.rows_pad + row;
+  float M = -INFINITY, Z = 0.f;
+  for (int c = 0; c < nch; c += 8) {
+    float2 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      v[u] = c + u < nch ? load_coherent(pp + (size_t)(c + u) * a.rows_pad)
+                         : make_float2(-INFINITY, 0.f);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float Mn = fmaxf(M, v[u].x);
+      if (Mn != -INFINITY) {
+        Z = Z * exp2f(M - Mn) + v[u].y * exp2f(v[u].x - Mn);
+        M = Mn;
+      }
+    }
+  }
+  store_row_lse<true>(a, s, lh, row, M, Z);
+}
+
+template <int D, int RG, bool CAUSAL>
+__global__ __launch_bounds__(kThreads, 2) void saliency_fused_kernel(SaliencyArgs a) {
+  using Sh = SweepShape<D, RG>;
+  __shared__ __attribute__((aligned(16))) uint8_t kbuf[Sh::RING_BYTES];
+  __shared__ float red[Sh::RED_FLOATS];
+  __shared__ int last;
+  const int LH = a.L * a.Hkv;
+  const int M = LH * a.total_chunks;
+  int pass, k;
+  fused_item((int)blockIdx.x, M, a.lag, pass, k);
+  pass = uniform(pass);
+  k = uniform(k);
+  const int lh = k / a.total_chunks, g = k - lh * a.total_chunks;
+  int s, c0;
+  locate_chunk(a, g, s, c0);
+  s = uniform(s);
+  c0 = uniform(c0);
+  const int nch = chunks_of(a, s);
+  int* cnt = a.unit_cnt + (size_t)s * LH + lh;
+  if (pass == 1) {
+    sweep<D, RG, 1, CAUSAL, true>(a, lh, g, kbuf, red, [] {});
+    // this wave's partials have reached device-coherent memory before the count moves
+    stores_done();
+    __syncthreads();
+    if (threadIdx.x == 0)
+      last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nch - 1;
+    __syncthreads();
+    if (!last) return;
+    merge_unit(a, s, lh, c0, nch);
+    stores_done();
+    __syncthreads();
+    if (threadIdx.x == 0) __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  } else {
+    // the chunk's first K tiles and Q are on their way while this waits
+    sweep<D, RG, 2, CAUSAL, true>(a, lh, g, kbuf, red, [&] {
+      if (threadIdx.x == 0) {
+        int spins = 0;
+        while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < nch + 1) {
+          __builtin_amdgcn_s_sleep(2);
+          if (++spins == kFusedSpins) {
+            if (a.status) atomicOr(a.status, kFlagSync);
+            break;
+          }
+        }
+      }
+      __syncthreads();
+    });
   }
 }
 
 // Merge the per-chunk (max, sum) partials of one (sequence, head) into the
-// log2-domain log-sum-exp of every window row. Padding rows and rows that see
-// no key get +inf, so that the second sweep gives them probability zero; the
-// natural-log value of every real row is exported when lse_out is set (-inf
-// for a row that sees no key).
+// log2-domain log-sum-exp of every window row (store_row_lse).
 // 1024 threads per (sequence, head): each row's chunks are split over
 // 1024 / rows_pad groups, each taking a max pass then a sum pass of
 // independent loads, and the groups are merged in LDS.
@@ -723,15 +970,7 @@ __global__ __launch_bounds__(kCombineThreads) void lse_combine_kernel(SaliencyAr
       M = Mn;
     }
   }
-  const bool seen = row < a.R && Z > 0.f;
-  const float l2 = seen ? M + log2f(Z) : INFINITY;
-  a.lse2[((size_t)s * LH + lh) * a.rows_pad + row] = l2;
-  if (a.lse_out && row < a.R) {
-    const int l = lh / a.Hkv, h = lh - l * a.Hkv;
-    const int w = (a.row0 + row) / a.G, g = (a.row0 + row) - w * a.G;
-    a.lse_out[(((size_t)l * a.S + s) * a.W + w) * a.Hq + h * a.G + g] =
-        seen ? l2 * 0.693147180559945309f : -INFINITY;
-  }
+  store_row_lse<false>(a, s, lh, row, M, Z);
 }
 
 // The caller's natural-log row LSE (lse_in [L][S][W][Hq]) in the layout and
@@ -755,6 +994,12 @@ template <int D, int RG, bool C>
 hipError_t launch_passes_c(const SaliencyArgs& a, SaliencyMode mode, hipStream_t st) {
   const int LH = a.L * a.Hkv;
   const unsigned grid = (unsigned)LH * (unsigned)a.total_chunks;
+  if (mode == SaliencyMode::kBoth && a.unit_cnt) {
+    const hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(a.unit_cnt), 0u, a.S * LH, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((saliency_fused_kernel<D, RG, C>), dim3(2 * grid), dim3(kThreads), 0, st, a);
+    return hipGetLastError();
+  }
   if (mode != SaliencyMode::kFromLse) {
     hipLaunchKernelGGL((saliency_kernel<D, RG, 1, C>), dim3(grid), dim3(kThreads), 0, st, a);
     hipLaunchKernelGGL(lse_combine_kernel, dim3(a.S * LH), dim3(kCombineThreads), 0, st, a);

@@ -372,7 +372,7 @@ def test_score_noalloc_rejects(lib):
     assert call(pb, scores=None) == B.EINVAL
     assert call(_problem(d=96)) == B.EUNSUPPORTED
     # 64 layers x 8 heads x 256 window rows over 64 sequences of 20000 tokens: the per-chunk
-    # partials alone exceed 32 MiB
+    # partials alone exceed the static scratch
     big = _problem(L=64, Hq=32, Hkv=8, W=64, cu=tuple(range(0, 64 * 20000 + 1, 20000)),
                    cu_steps=tuple(range(65)))
     assert lib.stepkv_saliency_workspace_bytes(ctypes.byref(big)) > B.STATIC_SCRATCH_BYTES

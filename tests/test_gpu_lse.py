@@ -16,6 +16,9 @@ pytestmark = pytest.mark.gpu
 
 CASES = {
     "tiny": dict(name="tiny"),
+    # d = 64 with W * G = 64 rows: 128-key tiles, several per chunk in every plan (16
+    # layers fill the chip with multi-tile chunks), both tiles of a barrier summed
+    "tiny_long": dict(name="tiny", num_layers=16, seqlens=[20000, 3001]),
     "l1_tail3001": dict(name="l1_8k", seqlens=[3001]),
     # short sequences: N = 1 and 130 < W * G rows; N = 0; a causal tail spanning tiles
     "ragged_g7": dict(name="ragged16", num_layers=2, seqlens=[2500, 700, 130, 1, 0, 4097],
