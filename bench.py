@@ -91,7 +91,11 @@ def parse():
     return ap.parse_args()
 
 
-SALIENCY_KERNELS = ("saliency_kernel", "lse_combine_kernel", "lse_import_kernel")
+# saliency-stage kernels: both sweeps in one launch (after its counters are cleared), or the
+# per-sweep kernels with the LSE combine or import (the one-launch name comes first: it does
+# not contain the per-sweep kernel's name)
+SALIENCY_KERNELS = ("saliency_fused_kernel", "saliency_kernel", "lse_combine_kernel",
+                    "lse_import_kernel", "fill_u32_kernel")
 
 
 def _saliency_part(name: str, lse_fed: bool):
@@ -140,7 +144,8 @@ def record_traffic(args) -> None:
             if k is None:
                 continue
             per_kernel[k].append(v * 1024.0 * cal)
-            launches += bool(re.search(r"saliency_kernel<\d+, \d+, 2[,>]", names[d]))
+            launches += bool(re.search(r"saliency_kernel<\d+, \d+, 2[,>]|saliency_fused_kernel<",
+                                       names[d]))
         out[counter] = {"calibration": cal, "launches": launches,
                         "bytes": sum(sum(v) for v in per_kernel.values()) / launches,
                         "per_kernel": {k: sum(v) / launches for k, v in per_kernel.items()}}

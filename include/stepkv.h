@@ -140,6 +140,14 @@ typedef struct stepkv_params {
    * observation prefill that yields T_i (App. C.2). A row that sees no key
    * (N_s < W - w) contributes nothing. */
   int32_t causal_tail;
+  /* schedule of the two saliency sweeps (0), a performance choice only (the
+   * results agree to rounding): 0 = chosen per problem: both sweeps in one
+   * launch, each key chunk's column sums about one round of workgroups after
+   * its row LSEs so that K is read again from the Infinity Cache, when K
+   * exceeds 192 MiB and there are at least twice as many chunks as resident
+   * workgroups, otherwise one launch per sweep; 1 = one launch per sweep;
+   * 2 = one launch. Calls given the row LSEs run one sweep either way. */
+  int32_t saliency_schedule;
 } stepkv_params;
 
 /* Per-step statistics of one (layer, KV head, step), from stepkv_score:

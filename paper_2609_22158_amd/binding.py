@@ -59,6 +59,7 @@ class ParamsC(ctypes.Structure):
         ("s_max", ctypes.c_float),
         ("eta", ctypes.c_float),
         ("causal_tail", ctypes.c_int32),
+        ("saliency_schedule", ctypes.c_int32),
     ]
 
 
@@ -198,6 +199,7 @@ class Params:
     s_max: float = 8.0
     eta: float = 1.5
     causal_tail: int = 0  # nonzero: window slot w sees keys 0 .. N - W + w only
+    saliency_schedule: int = 0  # 0 per problem, 1 one launch per sweep, 2 both in one launch
 
     def c(self) -> ParamsC:
         return ParamsC(*[getattr(self, f) for f, _ in ParamsC._fields_])

@@ -30,9 +30,6 @@ constexpr int kSalStartTiles = 6;
 // keep that window smaller but start more workgroups; 192 MiB (about 2300-key
 // chunks at d = 128) measured best on the 32k, 16k, ragged and last-query
 // workloads.
-#ifndef STEPKV_SAL_FUSED
-#define STEPKV_SAL_FUSED 1
-#endif
 constexpr int64_t kFusedReuseBytes = int64_t(192) << 20;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -76,6 +73,7 @@ struct SaliencyPlan {
   int R, rows_pad, chunk, total_chunks;
   // both sweeps in one launch: chunk, chunk count and row-LSE lead (items)
   int fused_chunk, fused_total_chunks, fused_lag;
+  bool fused_pays;  // the schedule chosen per problem (stepkv_params.saliency_schedule 0)
 };
 
 // Window rows per pair of sweeps (the MFMA tiling holds at most 256).
@@ -129,6 +127,11 @@ SaliencyPlan plan_saliency(const stepkv_problem* pb) {
     if (lead(c) * c * 2 * pb->head_dim <= kFusedReuseBytes) p.fused_chunk = c;
   p.fused_total_chunks = (int)chunks_for(p.fused_chunk);
   p.fused_lag = (int)std::min<int64_t>(lead(p.fused_chunk), lh * p.fused_total_chunks);
+  // One launch pays when K does not fit the reuse window anyway (otherwise the
+  // second of two launches already finds it in the Infinity Cache) and there
+  // are enough chunks for the row-LSE items to run a round ahead.
+  const int64_t k_bytes = lh * (int64_t)pb->cu_seqlens_host[pb->num_seqs] * 2 * pb->head_dim;
+  p.fused_pays = k_bytes > kFusedReuseBytes && lh * p.fused_total_chunks >= 2 * kSalSlots;
   return p;
 }
 
@@ -180,6 +183,7 @@ void stepkv_params_default(stepkv_params* p) {
   p->s_max = 8.0f;
   p->eta = 1.5f;
   p->causal_tail = 0;
+  p->saliency_schedule = 0;
 }
 
 const char* stepkv_strerror(int code) {
@@ -279,6 +283,7 @@ int check_params(const stepkv_problem* pb, const stepkv_params* prm) {
     return STEPKV_EINVAL;
   if (prm->pool_kernel < 1 || prm->pool_kernel % 2 == 0) return STEPKV_EINVAL;
   if (prm->pool_kernel > STEPKV_MAX_POOL_KERNEL) return STEPKV_EUNSUPPORTED;
+  if (prm->saliency_schedule < 0 || prm->saliency_schedule > 2) return STEPKV_EINVAL;
   if (window_rows(pb) > STEPKV_MAX_WINDOW_ROWS) return STEPKV_EUNSUPPORTED;
   return STEPKV_OK;
 }
@@ -317,7 +322,8 @@ int run_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void*
   sa.G = pb->num_q_heads / pb->num_kv_heads;
   sa.ntot = pb->cu_seqlens_host[pb->num_seqs];
   sa.status = pb->status;
-  const bool fused = STEPKV_SAL_FUSED != 0 && mode == SaliencyMode::kBoth;
+  const bool fused = mode == SaliencyMode::kBoth &&
+                     (prm->saliency_schedule == 0 ? plan.fused_pays : prm->saliency_schedule == 2);
   sa.chunk = fused ? plan.fused_chunk : plan.chunk;
   sa.total_chunks = fused ? plan.fused_total_chunks : plan.total_chunks;
   sa.unit_cnt = fused ? reinterpret_cast<int*>(ws + w.cnt) : nullptr;

@@ -148,6 +148,8 @@ def test_score_rejects_arguments(lib):
     assert _score(lib, pb, ws=FAKE * 16 + 8) == B.EWORKSPACE  # misaligned
     assert _score(lib, pb, prm=B.Params(pool_kernel=6).c()) == B.EINVAL
     assert _score(lib, pb, prm=B.Params(pool_kernel=65).c()) == B.EUNSUPPORTED
+    assert _score(lib, pb, prm=B.Params(saliency_schedule=3).c()) == B.EINVAL
+    assert _score(lib, pb, prm=B.Params(saliency_schedule=-1).c()) == B.EINVAL
     assert _score(lib, pb, prm=B.Params(alpha=float("nan")).c()) == B.EINVAL
     many = _problem(cu_steps=(0, 4097, 4099))
     assert _score(lib, many, stats=FAKE) == B.EUNSUPPORTED

@@ -71,6 +71,27 @@ def test_scores_and_saliency_match_oracle(cid):
             assert abs(A[l, h, a:b].sum() - w.window * w.group) < 1e-3 * w.window * w.group
 
 
+@pytest.mark.parametrize("schedule", [1, 2])
+@pytest.mark.parametrize("cid", ["tiny", "l32_32k_2l", "ragged_g7", "ragged_w64"])
+def test_both_sweep_schedules_match_oracle(cid, schedule):
+    """One launch per sweep (1) and both sweeps in one launch (2), whichever the
+    problem would get by itself: saliency and scores against the oracle, and the
+    one-launch path reports no stopped wait (STEPKV_FLAG_SYNC)."""
+    from paper_2609_22158_amd import binding as B
+
+    w, _, _, o = _case(cid)
+    g = HipRun(w, params=B.Params(saliency_schedule=schedule))
+    log(f"[schedule {schedule} {cid}]")
+    g.pb.status(clear=True)
+    sc = g.score(want_saliency=True)
+    P = sc["scores"].cpu().numpy()
+    A = sc["saliency"].cpu().numpy()
+    assert g.pb.status(clear=True) == 0
+    for s, l, h, a, b in _heads(w):
+        close(P[l, h, a:b], o["P"][(s, l, h)], f"P{(s, l, h)} schedule {schedule}")
+        close(A[l, h, a:b], o["A"][(s, l, h)], f"A{(s, l, h)} schedule {schedule}")
+
+
 def test_saliency_with_logit_spikes_matches_oracle():
     """Keys planted late in a key chunk lift one window row's logit by about
     40 and 90 nats above the rest of the row: the first exceeds fp32 exp range
