@@ -61,6 +61,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--lse-fed", action="store_true",
                     help="take the window rows' log-sum-exps as an input (one sweep over K)")
+    ap.add_argument("--schedule", type=int, choices=(0, 1, 2), default=0,
+                    help="saliency sweeps: 0 chosen per problem, 1 one launch per sweep, "
+                         "2 both in one launch (stepkv_params.saliency_schedule)")
     ap.add_argument("--causal-tail", action="store_true",
                     help="window slot w sees keys up to N - W + w only (causal prefill)")
     ap.add_argument("--text-signals", action="store_true",
@@ -334,12 +337,13 @@ def main():
     k_out = torch.empty((L, Hkv, out_rows, d), dtype=torch.bfloat16, device=dev)
     v_out = torch.empty_like(k_out)
     ws = torch.empty(pb.saliency_workspace_bytes(), dtype=torch.uint8, device=dev)
+    sched = dict(saliency_schedule=args.schedule)
     if args.selector == "token-only":
-        params = B.Params.token_only(causal_tail=int(args.causal_tail))
+        params = B.Params.token_only(causal_tail=int(args.causal_tail), **sched)
     elif args.selector == "last-query":
-        params = B.Params.last_query_only(causal_tail=int(args.causal_tail))
+        params = B.Params.last_query_only(causal_tail=int(args.causal_tail), **sched)
     else:
-        params = B.Params(causal_tail=int(args.causal_tail))
+        params = B.Params(causal_tail=int(args.causal_tail), **sched)
     stream = torch.cuda.current_stream()
     lse = None
     if args.lse_fed:  # stands for the prefill attention's row LSE, resident in HBM
@@ -610,7 +614,8 @@ def main():
                    "selector": args.selector,
                    "text_signals": bool(args.text_signals),
                    "shared_layers": n_sh if shared else 0,
-                   "saliency_sweeps": sweeps, "causal_tail": bool(args.causal_tail),
+                   "saliency_sweeps": sweeps, "saliency_schedule": args.schedule,
+                   "causal_tail": bool(args.causal_tail),
                    "layers": L, "kv_heads": Hkv, "q_heads": w.num_q_heads, "head_dim": d,
                    "seq_len": int(max(w.seqlens)), "tokens": int(ntot), "window": w.window,
                    "budget": budget, "seed": args.seed},

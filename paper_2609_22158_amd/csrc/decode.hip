@@ -303,7 +303,7 @@ void decode_mfma_kernel(DecodeArgs a) {
       __builtin_amdgcn_global_load_lds(
           static_cast<const void*>(vb + (size_t)rv * D + 8 * (vpiece ^ (2 * swz<D>(r)))),
           (__attribute__((address_space(3))) void*)(ring + slot * TB + i * (16 * kWave)), 16, 0,
-          0);
+          2);  // non-temporal, like the K loads: every row is read once
     }
   };
   auto compute = [&](int tt, auto slot_c) __attribute__((always_inline)) {
