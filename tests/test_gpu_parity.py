@@ -71,17 +71,20 @@ def test_scores_and_saliency_match_oracle(cid):
             assert abs(A[l, h, a:b].sum() - w.window * w.group) < 1e-3 * w.window * w.group
 
 
-@pytest.mark.parametrize("schedule", [1, 2])
+@pytest.mark.parametrize("schedule,causal", [(1, 0), (2, 0), (2, 1)])
 @pytest.mark.parametrize("cid", ["tiny", "l32_32k_2l", "ragged_g7", "ragged_w64"])
-def test_both_sweep_schedules_match_oracle(cid, schedule):
-    """One launch per sweep (1) and both sweeps in one launch (2), whichever the
-    problem would get by itself: saliency and scores against the oracle, and the
-    one-launch path reports no stopped wait (STEPKV_FLAG_SYNC)."""
+def test_both_sweep_schedules_match_oracle(cid, schedule, causal):
+    """One launch per sweep (1) and both sweeps in one launch (2, also with the
+    causal tail), whichever the problem would get by itself: saliency and scores
+    against the oracle, and the one-launch path reports no stopped wait
+    (STEPKV_FLAG_SYNC)."""
     from paper_2609_22158_amd import binding as B
 
     w, _, _, o = _case(cid)
-    g = HipRun(w, params=B.Params(saliency_schedule=schedule))
-    log(f"[schedule {schedule} {cid}]")
+    g = HipRun(w, params=B.Params(saliency_schedule=schedule, causal_tail=causal))
+    if causal:
+        o = run_oracle(w, g.budget, g.params)
+    log(f"[schedule {schedule} causal {causal} {cid}]")
     g.pb.status(clear=True)
     sc = g.score(want_saliency=True)
     P = sc["scores"].cpu().numpy()
