@@ -3,10 +3,14 @@
 // for every (sequence, layer, KV head), exactly, in two sweeps over K.
 //
 // The row softmax needs each row's log-sum-exp over all N keys before any
-// column can be summed, so the kernel runs
+// column can be summed, so the kernels run
 //   pass 1  per key chunk: z = K Q^T on MFMA, per-row running (max, sum exp)
 //   combine per row: merge the chunk partials into log2-domain LSE
 //   pass 2  per key chunk: z = Q K^T on MFMA, A_i = sum_r exp2(c z - lse_r)
+// either as three launches, or in one launch (saliency_fused_kernel) whose
+// column-sum chunks follow their head's row-LSE chunks about one round of
+// workgroups later, so that the second read of each chunk of K is served by
+// the Infinity Cache.
 // The two passes swap the MFMA operands so that each reduction stays inside
 // a lane: in pass 1 a lane holds 16 keys of one window row, in pass 2 16
 // window rows of one key (v_mfma_f32_32x32x16_bf16 output layout).
@@ -928,8 +932,8 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_fused_kernel(SaliencyArg
 // Merge the per-chunk (max, sum) partials of one (sequence, head) into the
 // log2-domain log-sum-exp of every window row (store_row_lse).
 // 1024 threads per (sequence, head): each row's chunks are split over
-// 1024 / rows_pad groups, each taking a max pass then a sum pass of
-// independent loads, and the groups are merged in LDS.
+// 1024 / rows_pad groups, each taking one online pass over its chunks with
+// eight loads in flight, and the groups are merged in LDS.
 constexpr int kCombineThreads = 1024;
 
 __global__ __launch_bounds__(kCombineThreads) void lse_combine_kernel(SaliencyArgs a) {
