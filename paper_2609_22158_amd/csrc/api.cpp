@@ -328,6 +328,16 @@ int run_saliency(const stepkv_problem* pb, const stepkv_params* prm, const void*
   sa.total_chunks = fused ? plan.fused_total_chunks : plan.total_chunks;
   sa.unit_cnt = fused ? reinterpret_cast<int*>(ws + w.cnt) : nullptr;
   sa.lag = plan.fused_lag;
+  // the chunk lookup's argument tables (used when S <= kArgSeqs)
+  int64_t chunks_before = 0;
+  for (int s = 0; s <= SaliencyArgs::kArgSeqs; ++s) {
+    const bool in = s <= pb->num_seqs;
+    sa.seq_first[s] = pb->cu_seqlens_host[in ? s : pb->num_seqs];
+    sa.chunk_first[s] = in ? (int)chunks_before : std::numeric_limits<int>::max();
+    if (s < pb->num_seqs)
+      chunks_before +=
+          (pb->cu_seqlens_host[s + 1] - pb->cu_seqlens_host[s] + sa.chunk - 1) / sa.chunk;
+  }
   const double scale = prm->scale > 0.0f ? (double)prm->scale : 1.0 / std::sqrt((double)d);
   sa.c = (float)(scale * 1.4426950408889634);  // log2(e)
   // Window rows in groups of at most 256, one pair of sweeps per group: a

@@ -33,6 +33,14 @@ struct SaliencyArgs {
   int* unit_cnt;
   int lag;
   uint32_t* status;  // device status word (STEPKV_FLAG_*) or null
+  // Batches of at most kArgSeqs sequences also pass cu_seqlens and each
+  // sequence's first chunk (at this launch's chunk size) by value: a workgroup
+  // then finds its chunk with scalar loads of its arguments, where a read of
+  // cu_seqlens would queue behind the K stream of the compute unit's other
+  // workgroup. Entries past S: seq_first = Ntot, chunk_first = INT_MAX.
+  static constexpr int kArgSeqs = 32;
+  int seq_first[kArgSeqs + 1];
+  int chunk_first[kArgSeqs + 1];
 };
 
 // Rows padded to whole row groups: 64, 128 or 256.

@@ -100,9 +100,16 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// Key chunks of sequence s: ceil(N_s / chunk).
-__device__ __forceinline__ int chunks_of(const SaliencyArgs& a, int s) {
+// Key chunks of sequence s: ceil(N_s / chunk), from cu_seqlens (s may differ
+// between lanes) ...
+__device__ __forceinline__ int chunks_in_memory(const SaliencyArgs& a, int s) {
   return (a.cu_seqlens[s + 1] - a.cu_seqlens[s] + a.chunk - 1) / a.chunk;
+}
+
+// ... or, for a wave-uniform s, from the argument tables when the batch has them.
+__device__ __forceinline__ int chunks_of(const SaliencyArgs& a, int s) {
+  if (a.S <= SaliencyArgs::kArgSeqs) return a.chunk_first[s + 1] - a.chunk_first[s];
+  return chunks_in_memory(a, s);
 }
 
 // The sequence s holding global chunk g (chunks of the sequences in order) and
@@ -116,7 +123,7 @@ __device__ __forceinline__ void locate_chunk(const SaliencyArgs& a, int g, int& 
   first_out = 0;
   for (int s0 = 0; s0 < a.S; s0 += kWave) {
     const int sq = s0 + lane;
-    const int cnt = sq < a.S ? chunks_of(a, sq) : 0;
+    const int cnt = sq < a.S ? chunks_in_memory(a, sq) : 0;
     int incl = cnt;
 #pragma unroll
     for (int off = 1; off < kWave; off <<= 1) {
@@ -134,12 +141,45 @@ __device__ __forceinline__ void locate_chunk(const SaliencyArgs& a, int g, int& 
   }
 }
 
+// Global chunk g (wave-uniform): its sequence s, the sequence's first global
+// chunk, first key and length. Batches of up to kArgSeqs sequences search the
+// argument tables (five scalar loads); larger ones take locate_chunk and read
+// cu_seqlens.
+struct ChunkLoc {
+  int s, first, seq0, ns;
+};
+
+__device__ __forceinline__ ChunkLoc find_chunk(const SaliencyArgs& a, int g) {
+  ChunkLoc r;
+  if (a.S <= SaliencyArgs::kArgSeqs) {
+    // the last s with chunk_first[s] <= g (a sequence without keys has no
+    // chunk, so the search passes over it)
+    int lo = 0;
+#pragma unroll
+    for (int step = SaliencyArgs::kArgSeqs / 2; step > 0; step >>= 1)
+      if (a.chunk_first[lo + step] <= g) lo += step;
+    r.s = lo;
+    r.first = a.chunk_first[lo];
+    r.seq0 = a.seq_first[lo];
+    r.ns = a.seq_first[lo + 1] - r.seq0;
+  } else {
+    locate_chunk(a, g, r.s, r.first);
+    r.s = uniform(r.s);
+    r.first = uniform(r.first);
+    // read into scalar registers: a value either branch may give stays scalar
+    r.seq0 = uniform(a.cu_seqlens[r.s]);
+    r.ns = uniform(a.cu_seqlens[r.s + 1]) - r.seq0;
+  }
+  return r;
+}
+
 // The first global chunk of sequence s: the chunks of the sequences before it.
 __device__ __forceinline__ int first_chunk(const SaliencyArgs& a, int s) {
+  if (a.S <= SaliencyArgs::kArgSeqs) return a.chunk_first[s];
   const int lane = threadIdx.x & 63;
   int acc = 0;
   for (int s0 = 0; s0 < s; s0 += kWave) {
-    int cnt = s0 + lane < s ? chunks_of(a, s0 + lane) : 0;
+    int cnt = s0 + lane < s ? chunks_in_memory(a, s0 + lane) : 0;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
     acc += cnt;
@@ -220,8 +260,8 @@ struct SweepShape {
 // the saliency the second sweep writes and the priority reads next.
 template <int D, int RG, int PASS, bool CAUSAL, bool FUSED, typename BeforeLse>
 __device__ __forceinline__ void sweep(const SaliencyArgs& a, int lh, const int rem_blk,
-                                      uint8_t* __restrict__ kbuf, float* __restrict__ red,
-                                      BeforeLse&& before_lse) {
+                                      const ChunkLoc& loc, uint8_t* __restrict__ kbuf,
+                                      float* __restrict__ red, BeforeLse&& before_lse) {
   using Sh = SweepShape<D, RG>;
   constexpr int KG = Sh::KG;
   constexpr int TILE = Sh::TILE;
@@ -246,13 +286,11 @@ __device__ __forceinline__ void sweep(const SaliencyArgs& a, int lh, const int r
 
   // ---- work item: (head lh, sequence s, chunk c)
   const int LH = a.L * a.Hkv;
-  int s, cfirst;
-  locate_chunk(a, rem_blk, s, cfirst);
-  s = uniform(s);
-  const int c = uniform(rem_blk - cfirst);
+  const int s = loc.s;
+  const int c = uniform(rem_blk - loc.first);
   const int l = lh / a.Hkv, h = lh - l * a.Hkv;
-  const int seq0 = a.cu_seqlens[s];
-  const int ns = a.cu_seqlens[s + 1] - seq0;
+  const int seq0 = loc.seq0;
+  const int ns = loc.ns;
   const int key0 = c * a.chunk;
   const int nkeys = min(a.chunk, ns - key0);
   const int ntiles = (nkeys + TILE - 1) / TILE;
@@ -791,7 +829,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_kernel(SaliencyArgs a) {
   int lh = blockIdx.x / a.total_chunks;
   const int g = blockIdx.x - lh * a.total_chunks;
   if (PASS == 2) lh = LH - 1 - lh;
-  sweep<D, RG, PASS, CAUSAL, false>(a, lh, g, kbuf, red, [] {});
+  sweep<D, RG, PASS, CAUSAL, false>(a, lh, g, find_chunk(a, g), kbuf, red, [] {});
 }
 
 // The log2-domain row LSE from a row's merged (max, sum): +inf for padding
@@ -892,14 +930,12 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_fused_kernel(SaliencyArg
   pass = uniform(pass);
   k = uniform(k);
   const int lh = k / a.total_chunks, g = k - lh * a.total_chunks;
-  int s, c0;
-  locate_chunk(a, g, s, c0);
-  s = uniform(s);
-  c0 = uniform(c0);
+  const ChunkLoc loc = find_chunk(a, g);
+  const int s = loc.s, c0 = loc.first;
   const int nch = chunks_of(a, s);
   int* cnt = a.unit_cnt + (size_t)s * LH + lh;
   if (pass == 1) {
-    sweep<D, RG, 1, CAUSAL, true>(a, lh, g, kbuf, red, [] {});
+    sweep<D, RG, 1, CAUSAL, true>(a, lh, g, loc, kbuf, red, [] {});
     // this wave's partials have reached device-coherent memory before the count moves
     stores_done();
     __syncthreads();
@@ -913,7 +949,7 @@ __global__ __launch_bounds__(kThreads, 2) void saliency_fused_kernel(SaliencyArg
     if (threadIdx.x == 0) __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   } else {
     // the chunk's first K tiles and Q are on their way while this waits
-    sweep<D, RG, 2, CAUSAL, true>(a, lh, g, kbuf, red, [&] {
+    sweep<D, RG, 2, CAUSAL, true>(a, lh, g, loc, kbuf, red, [&] {
       if (threadIdx.x == 0) {
         int spins = 0;
         while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < nch + 1) {

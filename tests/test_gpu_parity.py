@@ -27,6 +27,14 @@ CASES = {
     # W = 64 at G = 7: 448 window rows, two pairs of sweeps (256 and 192 rows)
     "ragged_w64": dict(name="ragged16", num_layers=2, window=64, seqlens=[1500, 333, 0, 2100],
                        protected_len=64),
+    # 32 sequences (the most whose chunk table the sweeps take as launch
+    # arguments) and 40 (found from cu_seqlens in device memory), with empty,
+    # one-token and multi-chunk sequences
+    "seqs32": dict(name="ragged16", num_layers=1, seqlens=[(53 * i + 7) % 600 for i in range(31)]
+                   + [4500], protected_len=64),
+    "seqs40": dict(name="ragged16", num_layers=1, seqlens=[(37 * i * i + 11 * i) % 700
+                                                           for i in range(39)] + [4500],
+                   protected_len=64),
 }
 
 _cache = {}
@@ -72,7 +80,7 @@ def test_scores_and_saliency_match_oracle(cid):
 
 
 @pytest.mark.parametrize("schedule,causal", [(1, 0), (2, 0), (2, 1)])
-@pytest.mark.parametrize("cid", ["tiny", "l32_32k_2l", "ragged_g7", "ragged_w64"])
+@pytest.mark.parametrize("cid", ["tiny", "l32_32k_2l", "ragged_g7", "ragged_w64", "seqs40"])
 def test_both_sweep_schedules_match_oracle(cid, schedule, causal):
     """One launch per sweep (1) and both sweeps in one launch (2, also with the
     causal tail), whichever the problem would get by itself: saliency and scores
