@@ -25,6 +25,12 @@ constexpr int rows_per_block() { return kThreads / (2 * D / 16) * kPasses; }
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
+// x[i] of an array that stays unchanged for the whole launch, read through the
+// constant address space: with a wave-uniform index the load is a scalar one.
+__device__ __forceinline__ int read_const(const int32_t* x, int i) {
+  return ((const __attribute__((address_space(4))) int32_t*)x)[i];
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   constexpr int kLanesPerRow = 2 * D / 16;
@@ -51,25 +57,44 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   const int32_t* __restrict__ idx = a.idx + (a.shared_idx ? 0 : in_head);
   // 1. every row's source position (independent index loads). When the
   // block's rows all belong to one sequence (always, but at sequence
-  // boundaries), that sequence is found once, in scalar registers.
+  // boundaries), that sequence and its bounds are found once, with scalar
+  // loads: vector loads of them would queue behind the K/V loads of the other
+  // blocks on the compute unit, and the index loads wait for them.
   const int o0 = rb * kRowsPerBlock;
   const int s0 = uniform(segment_of(a.cu_retained, a.S, max(min(o0, total - 1), 0)));
-  const bool one_seq = o0 >= a.cu_retained[s0] && o0 + kRowsPerBlock <= a.cu_retained[s0 + 1];
+  const int r0 = read_const(a.cu_retained, s0), r1 = read_const(a.cu_retained, s0 + 1);
+  const bool one_seq = o0 >= r0 && o0 + kRowsPerBlock <= r1;
   int src_row[kPasses];
   bool ok[kPasses];
+  if (one_seq) {
+    const int seq0 = read_const(a.cu_seqlens, s0), ns = read_const(a.cu_seqlens, s0 + 1) - seq0;
 #pragma unroll
-  for (int p = 0; p < kPasses; ++p) {
-    const int o = o0 + p * kRowsPerPass + sub;
-    ok[p] = false;
-    src_row[p] = 0;
-    if (o < total) {
-      const int s = one_seq ? s0 : segment_of(a.cu_retained, a.S, o);
-      const int j = o - a.cu_retained[s];
-      const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
-      if (j < ns) {
+    for (int p = 0; p < kPasses; ++p) {
+      const int o = o0 + p * kRowsPerPass + sub;
+      const int j = o - r0;
+      ok[p] = false;
+      src_row[p] = 0;
+      if (o < total && j < ns) {
         const int pos = idx[seq0 + j];
         ok[p] = pos >= 0 && pos < ns;  // not a valid position: row left untouched
         src_row[p] = ok[p] ? seq0 + pos : 0;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int p = 0; p < kPasses; ++p) {
+      const int o = o0 + p * kRowsPerPass + sub;
+      ok[p] = false;
+      src_row[p] = 0;
+      if (o < total) {
+        const int s = segment_of(a.cu_retained, a.S, o);
+        const int j = o - a.cu_retained[s];
+        const int seq0 = a.cu_seqlens[s], ns = a.cu_seqlens[s + 1] - seq0;
+        if (j < ns) {
+          const int pos = idx[seq0 + j];
+          ok[p] = pos >= 0 && pos < ns;
+          src_row[p] = ok[p] ? seq0 + pos : 0;
+        }
       }
     }
   }
