@@ -109,7 +109,10 @@ typedef struct stepkv_problem {
   int32_t head_dim;     /* d: 64 or 128 */
   int32_t window;       /* W >= 1 observation-window queries */
   int32_t num_seqs;     /* S >= 1 */
-  const int32_t* cu_seqlens_host; /* [S+1] host: 0 = cu[0] <= cu[1] <= ... */
+  const int32_t* cu_seqlens_host; /* [S+1] host: 0 = cu[0] <= cu[1] <= ... (read at
+                                     every call: it sizes the launches, and for S <= 32
+                                     the saliency sweeps take its values as launch
+                                     arguments; a captured graph keeps those) */
   const int32_t* cu_seqlens;      /* [S+1] device copy of the same values */
   const int32_t* cu_steps_host;   /* [S+1] host: offsets into step_utility */
   const int32_t* cu_steps;        /* [S+1] device copy of the same values */
