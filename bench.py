@@ -156,7 +156,8 @@ def record_traffic(args) -> None:
                         "bytes": sum(sum(v) for v in per_kernel.values()) / launches,
                         "per_kernel": {k: sum(v) / launches for k, v in per_kernel.items()}}
     budget = args.budget or 1024
-    key = traffic_key(args.workload, budget, args.window or 64, args.lse_fed)
+    key = traffic_key(args.workload, budget, args.window or 64, args.lse_fed, args.shared_layers,
+                      args.schedule)
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         db = json.load(open(path))
@@ -187,8 +188,14 @@ def source_digest() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def traffic_key(workload: str, budget: int, window: int, lse_fed: bool) -> str:
-    return f"{workload}_b{budget}_w{window}" + ("_lse" if lse_fed else "")
+def traffic_key(workload: str, budget: int, window: int, lse_fed: bool, shared_layers: int = 0,
+                schedule: int = 0) -> str:
+    """Key of a traffic record: the workload and every option that changes the
+    saliency launches (shared-index mode sweeps only its last layers; a forced
+    schedule may read K from HBM twice)."""
+    return (f"{workload}_b{budget}_w{window}" + ("_lse" if lse_fed else "")
+            + (f"_shared{shared_layers}" if shared_layers > 0 else "")
+            + (f"_schedule{schedule}" if schedule else ""))
 
 
 def recorded_traffic(key: str):
@@ -582,7 +589,8 @@ def main():
               else "saliency (two MFMA sweeps over K)")
     if shared:
         kernel = f"shared-index scoring: {kernel} of the last {n_sh} layers, head sum, priority"
-    traffic = recorded_traffic(traffic_key(args.workload, budget, w.window, args.lse_fed))
+    traffic = recorded_traffic(traffic_key(args.workload, budget, w.window, args.lse_fed,
+                                           n_sh if shared else 0, args.schedule))
     # the binding roofline: whichever of HBM and MFMA needs longer at peak
     if sal_bytes / (HBM_PEAK_GBS * 1e9) >= sal_flops / (BF16_PEAK_TFLOPS * 1e12):
         roofline = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS,
